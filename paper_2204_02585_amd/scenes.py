@@ -1,0 +1,243 @@
+"""Seeded synthetic inputs for the cached SqueezeNeRF renderer.
+
+This module only *makes inputs*: camera poses, intrinsics and the four cache
+arrays (three position sub-caches and the direction cache).  It holds none of
+the rendering arithmetic, so both the HIP path and the CPU oracle can consume
+what it produces without sharing any of the method's code.
+
+Cache layout (SqueezeNeRF Sec. 3.3, "Caching"): for each ordered pair
+j in {(x,y), (y,z), (z,x)} one dense n_p x n_p grid over the scene box holds
+sigma^j (1 value) and u^j, v^j, w^j (D values each), i.e. 3D+1 values per
+texel; the direction cache holds D values (beta) on an n_theta x n_phi grid.
+
+Array shapes produced here (the logical layout the C ABI accepts):
+  sigma[j] : [n_p][n_p]        plane j indexed [first axis][second axis]
+  uvw[j]   : [n_p][n_p][3D]    record = u[0..D) v[0..D) w[0..D)
+  beta     : [n_theta][n_phi][D]
+  poses    : [B][3][4] float32 camera-to-world [R | c], camera looks down -z
+
+Synthetic density: a sum of isotropic Gaussian blobs baked per plane.  A 3-D
+isotropic Gaussian factorises exactly into three planar Gaussians with twice
+the variance (exp(-|d|^2/2s^2) = prod_j exp(-(da^2+db^2)/4s^2)), so one blob
+is represented exactly by the product rule of Eq. 4; each planar factor is
+cut to exactly zero beyond a planar radius rho_b so that empty space is
+exactly empty.  The uvw components and beta are uniform in [-1, 1].
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import List, Optional
+
+import numpy as np
+
+BOX_MIN = (-1.5, -1.5, -1.5)
+BOX_MAX = (1.5, 1.5, 1.5)
+NEAR = 2.0
+FAR = 6.0
+
+# plane j -> (first axis, second axis), in the order xy, yz, zx
+PLANE_AXES = ((0, 1), (1, 2), (2, 0))
+
+
+@dataclasses.dataclass(frozen=True)
+class Config:
+    """One synthetic workload: image, sampling and cache shape."""
+    name: str
+    number: int              # seeds are derived from it (1000+n, 2000+n, ...)
+    width: int
+    height: int
+    n_samples: int
+    n_p: int
+    D: int
+    n_theta: int
+    n_phi: int
+    dtype: str               # "f32" or "f16" storage for sigma, uvw and beta
+    n_blobs: int
+    sigma_max: float
+    r_min: float
+    r_max: float
+    n_poses: int = 1
+    stratified: bool = False
+    t_eps: float = 1e-4
+    focal: Optional[float] = None  # default 1.25 * width
+
+    @property
+    def fx(self) -> float:
+        return float(self.focal if self.focal is not None else 1.25 * self.width)
+
+    @property
+    def nominal_samples(self) -> int:
+        """Samples per call: one ray per pixel, N samples per ray, B views."""
+        return self.width * self.height * self.n_samples * self.n_poses
+
+
+CONFIGS = {
+    # 64x64, N=64, k=64, D=8, all fp32, direction cache 32x32
+    "tiny": Config("tiny", 1, 64, 64, 64, 64, 8, 32, 32, "f32", 16, 50.0, 0.1, 0.4,
+                   focal=80.0),
+    # 800x800, N=192, k=256, D=8, fp16, direction cache 128x128
+    "paper": Config("paper", 2, 800, 800, 192, 256, 8, 128, 128, "f16", 64, 50.0, 0.1, 0.4),
+    # as "paper" with k=1024, direction cache 384x384, denser blobs
+    "large": Config("large", 3, 800, 800, 192, 1024, 8, 384, 384, "f16", 64, 200.0, 0.1, 0.4),
+    # 100 views on a spiral, caches as "paper"
+    "batch": Config("batch", 4, 800, 800, 192, 256, 8, 128, 128, "f16", 64, 50.0, 0.1, 0.4,
+                    n_poses=100),
+    # 1920x1080, N=384 stratified, k=2048, D=16, direction cache 512x512
+    "stress": Config("stress", 5, 1920, 1080, 384, 2048, 16, 512, 512, "f16", 256, 50.0,
+                     0.02, 0.5, stratified=True),
+}
+
+
+def look_at_pose(radius: float, azimuth_deg: float, elevation_deg: float) -> np.ndarray:
+    """Camera-to-world [R | c] (float32, 3x4) for a camera on a sphere around
+    the origin looking at it, world up = +z; camera axes: +x right, +y up,
+    looking down -z."""
+    az = math.radians(azimuth_deg)
+    el = math.radians(elevation_deg)
+    c = np.array([radius * math.cos(el) * math.cos(az),
+                  radius * math.cos(el) * math.sin(az),
+                  radius * math.sin(el)], dtype=np.float64)
+    fwd = -c / np.linalg.norm(c)
+    right = np.cross(fwd, np.array([0.0, 0.0, 1.0]))
+    right /= np.linalg.norm(right)
+    up = np.cross(right, fwd)
+    pose = np.zeros((3, 4), dtype=np.float64)
+    pose[:, 0] = right
+    pose[:, 1] = up
+    pose[:, 2] = -fwd
+    pose[:, 3] = c
+    return pose.astype(np.float32)
+
+
+def single_pose() -> np.ndarray:
+    """The one view of the single-camera workloads: radius 4, azimuth 45 deg,
+    elevation 30 deg."""
+    return look_at_pose(4.0, 45.0, 30.0)[None]
+
+
+def spiral_poses(n: int, seed: int = 5000) -> np.ndarray:
+    """n views on a seeded spiral: radius 3.5..4.5, elevation -30..30 deg."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    a0 = rng.uniform(0.0, 2.0 * math.pi)
+    out = np.zeros((n, 3, 4), dtype=np.float32)
+    for k in range(n):
+        s = k / (n - 1) if n > 1 else 0.0
+        r = 4.0 + 0.5 * math.cos(6.0 * math.pi * s)
+        el = 30.0 * math.sin(2.0 * math.pi * s)
+        az = math.degrees(a0 + 4.0 * math.pi * s)
+        out[k] = look_at_pose(r, az, el)
+    return out
+
+
+@dataclasses.dataclass
+class Blobs:
+    centre: np.ndarray   # [n][3]
+    radius: np.ndarray   # [n]
+    sigma_max: float
+
+
+def make_blobs(n: int, sigma_max: float, r_min: float, r_max: float, seed: int) -> Blobs:
+    rng = np.random.Generator(np.random.PCG64(seed))
+    centre = rng.uniform(-1.0, 1.0, size=(n, 3))
+    radius = rng.uniform(r_min, r_max, size=n)
+    return Blobs(centre, radius, float(sigma_max))
+
+
+def node_coords(n_p: int, lo: float, hi: float) -> np.ndarray:
+    """Vertex-aligned grid nodes spanning [lo, hi] (both faces included)."""
+    return lo + np.arange(n_p, dtype=np.float64) * ((hi - lo) / (n_p - 1))
+
+
+def bake_sigma_planes(n_p: int, blobs: Blobs, dtype=np.float32,
+                      bmin=BOX_MIN, bmax=BOX_MAX,
+                      s_frac: float = 0.25, rho_frac: float = 0.6) -> List[np.ndarray]:
+    """Per-plane density factors: sum over blobs of
+    sigma_max^(1/3) * exp(-(da^2 + db^2) / (4 s^2)), cut to 0 beyond rho."""
+    amp = blobs.sigma_max ** (1.0 / 3.0)
+    planes = []
+    for (ra, rb) in PLANE_AXES:
+        xa = node_coords(n_p, bmin[ra], bmax[ra])
+        xb = node_coords(n_p, bmin[rb], bmax[rb])
+        acc = np.zeros((n_p, n_p), dtype=np.float64)
+        step_a = (bmax[ra] - bmin[ra]) / (n_p - 1)
+        step_b = (bmax[rb] - bmin[rb]) / (n_p - 1)
+        for c, r in zip(blobs.centre, blobs.radius):
+            s = s_frac * r
+            rho = rho_frac * r
+            ca, cb = c[ra], c[rb]
+            a0 = max(0, int(math.floor((ca - rho - bmin[ra]) / step_a)))
+            a1 = min(n_p - 1, int(math.ceil((ca + rho - bmin[ra]) / step_a)))
+            b0 = max(0, int(math.floor((cb - rho - bmin[rb]) / step_b)))
+            b1 = min(n_p - 1, int(math.ceil((cb + rho - bmin[rb]) / step_b)))
+            if a0 > a1 or b0 > b1:
+                continue
+            da = xa[a0:a1 + 1, None] - ca
+            db = xb[None, b0:b1 + 1] - cb
+            r2 = da * da + db * db
+            f = amp * np.exp(-r2 / (4.0 * s * s))
+            f[r2 > rho * rho] = 0.0
+            acc[a0:a1 + 1, b0:b1 + 1] += f
+        planes.append(acc.astype(dtype))
+    return planes
+
+
+def uniform_pm1(shape, dtype, rng: np.random.Generator, chunk_rows: int = 64) -> np.ndarray:
+    """Values uniform in [-1, 1], rounded once from float32 to `dtype`,
+    generated in row chunks so that large caches never hold float64 copies."""
+    out = np.empty(shape, dtype=dtype)
+    rows = shape[0]
+    for r0 in range(0, rows, chunk_rows):
+        r1 = min(rows, r0 + chunk_rows)
+        v = rng.random(size=(r1 - r0,) + tuple(shape[1:]), dtype=np.float32)
+        v *= 2.0
+        v -= 1.0
+        out[r0:r1] = v.astype(dtype)
+    return out
+
+
+def np_dtype(name: str):
+    return {"f32": np.float32, "f16": np.float16}[name]
+
+
+@dataclasses.dataclass
+class Scene:
+    """Everything one render call needs, as host arrays."""
+    config: Config
+    sigma: List[np.ndarray]
+    uvw: List[np.ndarray]
+    beta: np.ndarray
+    poses: np.ndarray
+    near: float = NEAR
+    far: float = FAR
+    bbox_min: tuple = BOX_MIN
+    bbox_max: tuple = BOX_MAX
+    seed: int = 0
+
+    @property
+    def intrinsics(self):
+        c = self.config
+        return dict(fx=c.fx, fy=c.fx, cx=c.width / 2.0, cy=c.height / 2.0,
+                    width=c.width, height=c.height)
+
+    def cache_nbytes(self) -> int:
+        return (sum(a.nbytes for a in self.sigma) + sum(a.nbytes for a in self.uvw)
+                + self.beta.nbytes)
+
+
+def make_scene(name_or_config, n_poses: Optional[int] = None) -> Scene:
+    """Build the seeded inputs of one named workload ("tiny", "paper",
+    "large", "batch", "stress") or of a Config."""
+    cfg = CONFIGS[name_or_config] if isinstance(name_or_config, str) else name_or_config
+    if n_poses is not None:
+        cfg = dataclasses.replace(cfg, n_poses=n_poses)
+    n = cfg.number
+    dt = np_dtype(cfg.dtype)
+    blobs = make_blobs(cfg.n_blobs, cfg.sigma_max, cfg.r_min, cfg.r_max, 1000 + n)
+    sigma = bake_sigma_planes(cfg.n_p, blobs, dt)
+    rng_uvw = np.random.Generator(np.random.PCG64(2000 + n))
+    uvw = [uniform_pm1((cfg.n_p, cfg.n_p, 3 * cfg.D), dt, rng_uvw) for _ in range(3)]
+    rng_beta = np.random.Generator(np.random.PCG64(3000 + n))
+    beta = uniform_pm1((cfg.n_theta, cfg.n_phi, cfg.D), dt, rng_beta)
+    poses = single_pose() if cfg.n_poses == 1 else spiral_poses(cfg.n_poses)
+    return Scene(cfg, sigma, uvw, beta, poses, seed=4000 + n)

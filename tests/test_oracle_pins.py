@@ -1,0 +1,419 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+Each test names the passage (or the reading of it) it pins.  Expected values
+are hand-derived in the comments; none comes from the oracle or the HIP path.
+"""
+import math
+import os
+from decimal import Decimal, getcontext
+
+import numpy as np
+import pytest
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+FNV_OFFSET = 2166136261
+FNV_PRIME = 16777619
+
+
+def fnv1a(words):
+    """FNV-1a 32-bit over little-endian 32-bit words (the hash definition)."""
+    h = FNV_OFFSET
+    for w in words:
+        for k in range(4):
+            h ^= (w >> (8 * k)) & 0xFF
+            h = (h * FNV_PRIME) & 0xFFFFFFFF
+    return h
+
+
+def sigmoid(x):
+    return 1.0 / (1.0 + math.exp(-x))
+
+
+def centre_ray_pose(direction, origin):
+    """3x4 camera-to-world whose centre-pixel ray has direction exactly
+    `direction` (the pose's third column is -direction)."""
+    P = np.zeros((1, 3, 4), dtype=np.float32)
+    P[0, :, 2] = -np.asarray(direction, dtype=np.float32)
+    P[0, :, 3] = origin
+    return P
+
+
+# a 1x1 image whose only pixel centre sits on the principal point
+ONE_PIXEL = dict(fx=1.0, fy=1.0, cx=0.5, cy=0.5, width=1, height=1)
+
+
+def const_planes(n_p, values, dtype=np.float32):
+    return [np.full((n_p, n_p), v, dtype=dtype) for v in values]
+
+
+def uvw_const(n_p, D, per_plane, dtype=np.float32):
+    """per_plane[j] = (u, v, w) scalars broadcast over D and the grid."""
+    out = []
+    for (u, v, w) in per_plane:
+        rec = np.concatenate([np.full(D, u), np.full(D, v), np.full(D, w)]).astype(dtype)
+        out.append(np.broadcast_to(rec, (n_p, n_p, 3 * D)).copy())
+    return out
+
+
+def beta_const(value, D=1, n_theta=2, n_phi=2, dtype=np.float32):
+    return np.full((n_theta, n_phi, D), value, dtype=dtype)
+
+
+# --------------------------------------------------------------------------
+# Sec. 3.3 / Sec. 1: storage formula and the work unit
+# --------------------------------------------------------------------------
+
+def _golden_printed():
+    vals = {}
+    with open(os.path.join(GOLDEN, "paper_printed.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                k, v, _ = line.split()
+                vals[k] = float(v)
+    return vals
+
+
+def test_cache_size_formula_matches_printed_sizes():
+    """Sec. 3.3: 3 n_p^2 (3D+1) values (sigma fp32, uvw fp16) plus n_d^2 D
+    (beta fp16) gives the printed 39MB (512 cache) and 155MB (1K cache)."""
+    g = _golden_printed()
+    mib = 1024.0 * 1024.0
+    b512 = oracle.cache_nbytes(512, 8, 64, 64, 4, 2, 2)
+    assert b512 == 40_960_000
+    assert abs(b512 / mib - g["cache_mb_np512_nd64_D8"]) < 0.1
+    assert abs(b512 / 1e6 - g["cache_mb_approx_np512"]) < 1.0
+    b1k = oracle.cache_nbytes(1024, 8, 64, 64, 4, 2, 2)
+    assert abs(b1k / mib - g["cache_mb_np1024_nd64_D8"]) / g["cache_mb_np1024_nd64_D8"] < 0.01
+
+
+def test_work_unit_matches_printed_sample_count():
+    """Sec. 1: 800x800 pixels x 192 samples = 122.88 million queries."""
+    from paper_2204_02585_amd import scenes
+    g = _golden_printed()
+    assert scenes.CONFIGS["paper"].nominal_samples == int(g["samples_800x800x192"])
+
+
+# --------------------------------------------------------------------------
+# input decoding and generators
+# --------------------------------------------------------------------------
+
+def test_half_decoding_matches_library_on_all_patterns():
+    bits = np.arange(65536, dtype=np.uint16)
+    ref = bits.view(np.float16).astype(np.float64)
+    got = np.array([oracle.half_to_double(int(b)) for b in bits])
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+
+
+def test_splitmix64_published_sequence():
+    with open(os.path.join(GOLDEN, "splitmix64_seed0.txt")) as f:
+        want = [int(l, 16) for l in f if l.strip() and not l.startswith("#")]
+    assert [oracle.splitmix64(0, c) for c in range(len(want))] == want
+
+
+def test_tau_eps_matches_high_precision_log():
+    """T >= eps <=> sum sigma delta <= -ln eps (Eq. 1's T_i), as a 2^-32
+    fixed-point bound."""
+    getcontext().prec = 60
+    for eps in (1e-4, 1e-3, 0.5, 1e-7):
+        e = Decimal(float(np.float32(eps)))
+        want = int((-e.ln()) * (2 ** 32))
+        assert abs(oracle.tau_eps_q(eps) - want) <= 1
+    assert oracle.tau_eps_q(0.0) == 2 ** 63 - 1
+
+
+# --------------------------------------------------------------------------
+# Eq. 4 + Sec. 3.4: plane order, nearest-neighbour rounding, box boundary
+# --------------------------------------------------------------------------
+
+# Scene for the axis-ray cases: box [-1,1]^3, n_p = 3 so nodes sit at
+# -1, 0, 1 and the grid scale is exactly 1.  Near 1, far 5, N = 8, so
+# t_i = 1 + i/2 and the ray coordinate along its axis is -3 + t_i:
+#   i      0    1    2    3    4    5    6    7
+#   coord -2  -1.5  -1  -0.5   0   0.5   1   1.5
+#   inside  n    n    y    y    y    y    y    n      (both faces included)
+#   g            .    0   0.5   1   1.5   2           (g = coord + 1)
+#   node         .    0    1    1    2    2           (ties round up)
+# The varied plane holds (1 + 3a + b)/4 at [a][b]; the other two hold 1.
+# The fixed coordinates are 0.5 (g = 1.5 -> node 2, a tie) and -0.25
+# (g = 0.75 -> node 1).  Looked-up values: [2][0]=7/4, [2][1]=2, [2][1]=2,
+# [2][2]=9/4, [2][2]=9/4, each over delta = 1/2, so q = 7/8, 1, 1, 9/8, 9/8
+# and the optical depths before samples 2..7 are 0, 7/8, 15/8, 23/8, 4, 41/8.
+
+AXIS_Q = [0.875, 1.0, 1.0, 1.125, 1.125]
+AXIS_T = [2.0, 2.5, 3.0, 3.5, 4.0]
+
+
+def _axis_expected(n_live=5):
+    tau = 0.0
+    acc = depth = 0.0
+    for q, t in zip(AXIS_Q[:n_live], AXIS_T[:n_live]):
+        w = math.exp(-tau) * (1.0 - math.exp(-q))
+        acc += w
+        depth += w * t
+        tau += q
+    return acc, depth, tau
+
+
+def _pattern(n_p=3):
+    a = np.arange(n_p)[:, None]
+    b = np.arange(n_p)[None, :]
+    return ((1 + 3 * a + b) / 4.0).astype(np.float32)
+
+
+AXIS_CASES = {
+    # varied plane, ray direction, origin, (ix, iy, iz) sequence over i = 2..6
+    "xy": (0, (0, 1, 0), (0.5, -3.0, -0.25), [(2, 0, 1), (2, 1, 1), (2, 1, 1), (2, 2, 1), (2, 2, 1)]),
+    "yz": (1, (0, 0, 1), (-0.25, 0.5, -3.0), [(1, 2, 0), (1, 2, 1), (1, 2, 1), (1, 2, 2), (1, 2, 2)]),
+    "zx": (2, (1, 0, 0), (-3.0, -0.25, 0.5), [(0, 1, 2), (1, 1, 2), (1, 1, 2), (2, 1, 2), (2, 1, 2)]),
+}
+
+
+def _render_axis(case, t_eps=0.0, dtype=np.float32, uvw=None, beta=None, D=1):
+    j, direction, origin, _ = AXIS_CASES[case]
+    sigma = const_planes(3, (1.0, 1.0, 1.0), dtype)
+    sigma[j] = _pattern().astype(dtype)
+    if uvw is None:
+        uvw = uvw_const(3, D, [(0, 0, 0)] * 3, dtype)
+    if beta is None:
+        beta = beta_const(0.0, D=D, dtype=dtype)
+    return oracle.render(sigma, uvw, beta, centre_ray_pose(direction, origin), ONE_PIXEL,
+                         1.0, 5.0, 8, (-1, -1, -1), (1, 1, 1), t_eps=t_eps)[0]
+
+
+@pytest.mark.parametrize("case", sorted(AXIS_CASES))
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_plane_order_rounding_and_box(case, dtype):
+    r = _render_axis(case, dtype=dtype)
+    acc, depth, tau = _axis_expected()
+    assert r["stop"] == 8 and r["n_inbox"] == 5 and r["n_occ"] == 5
+    assert r["tau_end"] == int(tau * 2 ** 32)            # 41/8, exact
+    assert abs(r["acc"] - acc) < 1e-12
+    assert abs(r["depth"] - depth) < 1e-12
+    # beta = 0: every colour is sigmoid(0) = 1/2
+    assert np.allclose(r["rgb"], 0.5 * acc, atol=1e-12, rtol=0)
+    idx = AXIS_CASES[case][3]
+    words = []
+    for i, (ix, iy, iz) in zip(range(2, 7), idx):
+        words += [i, ix, iy, iz]
+    assert r["hash"] == fnv1a(words)
+
+
+def test_termination_stops_after_threshold():
+    """Early termination (T_i < eps): with eps = e^-2.5 the optical depths
+    0, 7/8, 15/8, 23/8 before samples 2..5 leave samples 2, 3, 4 live and stop
+    at sample 5."""
+    r = _render_axis("xy", t_eps=math.exp(-2.5))
+    acc, depth, tau = _axis_expected(n_live=3)
+    assert r["stop"] == 5 and r["n_inbox"] == 3 and r["n_occ"] == 3
+    assert r["tau_end"] == int(tau * 2 ** 32)
+    assert abs(r["acc"] - acc) < 1e-12 and abs(r["depth"] - depth) < 1e-12
+
+
+def test_fusion_sums_uvw_over_planes():
+    """Eq. 4 (k = k^xy + k^yz + k^zx) and Eq. 2 with D = 1, beta = 1:
+    c = sigmoid(U, V, W).  Planes: u = (0.5, 0.25, -0.125) -> 0.625,
+    v = (1, -1, 0.5) -> 0.5, w = (-0.5, -0.25, -0.25) -> -1."""
+    uvw = uvw_const(3, 1, [(0.5, 1.0, -0.5), (0.25, -1.0, -0.25), (-0.125, 0.5, -0.25)])
+    r = _render_axis("xy", uvw=uvw, beta=beta_const(1.0))
+    acc, _, _ = _axis_expected()
+    want = np.array([sigmoid(0.625), sigmoid(0.5), sigmoid(-1.0)]) * acc
+    assert np.allclose(r["rgb"], want, atol=1e-12, rtol=0)
+
+
+def test_inner_product_over_D_components():
+    """Eq. 2 with D = 3: c_r = sum_d beta_d u_d.  beta = (1, -2, 0.5) on
+    every direction node, u^xy = (0.25, 0.5, 1) on every texel, other planes
+    0: x = 0.25 - 1 + 0.5 = -0.25 for every channel."""
+    D = 3
+    rec = np.array([0.25, 0.5, 1.0] * 3, dtype=np.float32)
+    uvw = [np.broadcast_to(rec, (3, 3, 9)).copy(), np.zeros((3, 3, 9), np.float32),
+           np.zeros((3, 3, 9), np.float32)]
+    beta = np.broadcast_to(np.array([1.0, -2.0, 0.5], np.float32), (2, 2, D)).copy()
+    r = _render_axis("xy", uvw=uvw, beta=beta, D=D)
+    acc, _, _ = _axis_expected()
+    assert np.allclose(r["rgb"], sigmoid(-0.25) * acc, atol=1e-12, rtol=0)
+
+
+# --------------------------------------------------------------------------
+# Eq. 1: closed forms for uniform density
+# --------------------------------------------------------------------------
+
+def test_uniform_density_opacity_and_depth_closed_form():
+    """Uniform sigma over a segment of length L has opacity 1 - exp(-sigma L)
+    (Eq. 1 telescopes).  Pinhole geometry: |d| = sqrt(a^2 + b^2 + 1) with
+    a = (u + 1/2 - cx)/fx, b = (v + 1/2 - cy)/fy, so L = (far - near)|d|.
+    With q = sigma dt |d| per sample, depth = sum_i e^{-iq}(1 - e^{-q}) t_i."""
+    from paper_2204_02585_amd import scenes
+    sig = 0.75
+    n_p, W, H, N, near, far = 2, 5, 4, 48, 2.0, 6.0
+    intr = dict(fx=6.0, fy=6.0, cx=2.5, cy=2.0, width=W, height=H)
+    pose = scenes.look_at_pose(4.0, 30.0, 20.0)[None]
+    out = oracle.render(const_planes(n_p, (sig, 1.0, 1.0)), uvw_const(n_p, 1, [(0, 0, 0)] * 3),
+                        beta_const(0.0), pose, intr, near, far, N,
+                        (-100, -100, -100), (100, 100, 100), t_eps=0.0)
+    for v in range(H):
+        for u in range(W):
+            r = out[v * W + u]
+            a = (u + 0.5 - intr["cx"]) / intr["fx"]
+            b = (v + 0.5 - intr["cy"]) / intr["fy"]
+            dn = math.sqrt(a * a + b * b + 1.0)
+            L = (far - near) * dn
+            assert abs(r["acc"] - (1.0 - math.exp(-sig * L))) < 2e-6
+            q = sig * (far - near) / N * dn
+            depth = sum(math.exp(-i * q) * (1 - math.exp(-q)) * (near + i * (far - near) / N)
+                        for i in range(N))
+            assert abs(r["depth"] - depth) < 2e-5
+            assert np.allclose(r["rgb"], 0.5 * r["acc"], atol=1e-15, rtol=0)
+            assert r["stop"] == N and r["n_occ"] == N
+
+
+def test_termination_index_for_uniform_density():
+    """Uniform q per sample: samples are live while i * Q <= tau_eps, so the
+    ray stops at floor(tau_eps / Q) + 1.  sigma = 16, dt = 1/32, |d| = 1 ->
+    q = 1/2, Q = 2^31; eps = 1e-4 -> tau_eps = 39558110791 -> stop = 19."""
+    N = 64
+    r = oracle.render(const_planes(2, (16.0, 1.0, 1.0)), uvw_const(2, 1, [(0, 0, 0)] * 3),
+                      beta_const(0.0), centre_ray_pose((0, 1, 0), (0, 0, 0)), ONE_PIXEL,
+                      2.0, 4.0, N, (-100, -100, -100), (100, 100, 100), t_eps=1e-4)[0]
+    Q = 2 ** 31
+    assert r["stop"] == oracle.tau_eps_q(1e-4) // Q + 1 == 19
+    assert r["tau_end"] == 19 * Q
+    assert abs(r["acc"] - (1 - math.exp(-9.5))) < 1e-9
+
+
+def test_stratified_first_interval_starts_at_jittered_sample():
+    """Stratified sampling: t_0 = near + xi_0 dt with xi_0 from the first
+    SplitMix64 output of seed 0 (ray 0, sample 0), and the intervals
+    telescope to far - t_0, so opacity = 1 - exp(-sigma (far - t_0))."""
+    h0 = 0xE220A8397B1DCDAF
+    xi0 = (h0 >> 40) / 2.0 ** 24
+    near, far, N, sig = 2.0, 4.0, 16, 0.5
+    dt = np.float32((far - near) / N)
+    t0 = float(np.float32(near) + np.float32(np.float32(xi0) * dt))
+    r = oracle.render(const_planes(2, (sig, 1.0, 1.0)), uvw_const(2, 1, [(0, 0, 0)] * 3),
+                      beta_const(0.0), centre_ray_pose((0, 1, 0), (0, 0, 0)), ONE_PIXEL,
+                      near, far, N, (-100, -100, -100), (100, 100, 100), t_eps=0.0,
+                      stratified=True, seed=0)[0]
+    assert abs(r["acc"] - (1 - math.exp(-sig * (far - t0)))) < 1e-6
+
+
+# --------------------------------------------------------------------------
+# Sec. 3.4: bilinear direction lookup over (theta, phi)
+# --------------------------------------------------------------------------
+
+# n_theta = 3 nodes at theta = 0, pi/2, pi; n_phi = 4 periodic nodes at
+# phi = -pi, -pi/2, 0, pi/2.  Node [a][b] holds 10a + b - 5 (distinct).
+def _beta_nodes():
+    a = np.arange(3)[:, None, None]
+    b = np.arange(4)[None, :, None]
+    return ((10 * a + b - 5) / 16.0).astype(np.float32)
+
+
+B = _beta_nodes()[..., 0].astype(np.float64)
+DIRECTION_CASES = [
+    # direction, expected beta (hand-derived from theta, phi)
+    ((1, 0, 0), B[1, 2]),                        # theta pi/2, phi 0: a node
+    ((1, 1, 0), (B[1, 2] + B[1, 3]) / 2),        # phi pi/4: halfway in phi
+    ((-1, 1, 0), (B[1, 3] + B[1, 0]) / 2),       # phi 3pi/4: wraps pi -> -pi
+    ((-1, 0, 0), B[1, 0]),                       # phi = pi is node -pi
+    ((0, -1, 0), B[1, 1]),                       # phi -pi/2
+    ((1, 0, 1), (B[0, 2] + B[1, 2]) / 2),        # theta pi/4: halfway in theta
+    ((0, 0, -1), B[2, 2]),                       # theta = pi clamps to last row
+]
+
+
+@pytest.mark.parametrize("direction,want", DIRECTION_CASES)
+def test_direction_bilinear_lookup(direction, want):
+    """With D = 1, u = v = w = 1 and uniform sigma, every sample has colour
+    sigmoid(beta(d)), so rgb / acc = sigmoid(beta)."""
+    r = oracle.render(const_planes(2, (2.0, 1.0, 1.0)), uvw_const(2, 1, [(1, 1, 1), (0, 0, 0), (0, 0, 0)]),
+                      _beta_nodes(), centre_ray_pose(direction, (0, 0, 0)), ONE_PIXEL,
+                      2.0, 4.0, 8, (-100, -100, -100), (100, 100, 100), t_eps=0.0)[0]
+    assert r["acc"] > 0.9
+    assert np.allclose(r["rgb"] / r["acc"], sigmoid(want), atol=1e-12, rtol=0)
+
+
+# --------------------------------------------------------------------------
+# camera conventions (readings: +x right, +y up, looking down -z, v=0 top)
+# --------------------------------------------------------------------------
+
+def test_image_orientation():
+    """A camera at the origin looking along +y with up +z: the top pixel row
+    (v = 0) looks upward and sees only the z > 0 half space; the right
+    column (u = 1) sees only the x > 0 half space."""
+    from paper_2204_02585_amd import scenes
+    P = np.zeros((1, 3, 4), np.float32)
+    P[0, :, 0] = (1, 0, 0)     # right
+    P[0, :, 1] = (0, 0, 1)     # up
+    P[0, :, 2] = (0, -1, 0)    # back (camera looks along +y)
+    intr = dict(fx=2.0, fy=2.0, cx=1.0, cy=1.0, width=2, height=2)
+    # box [-4,4]^3 with 9 nodes: node 5 and up are z (or x) >= 1/2; the
+    # rays leave the axis with slope 1/4, so they reach |z| = 1 at t = 4
+    n_p = 9
+    upper = np.zeros((n_p, n_p), np.float32)
+    upper[:, 5:] = 4.0                           # Syz[iy][iz]: z > 0 only
+    right = np.zeros((n_p, n_p), np.float32)
+    right[:, 5:] = 4.0                           # Szx[iz][ix]: x > 0 only
+    ones = np.ones((n_p, n_p), np.float32)
+    u0 = uvw_const(n_p, 1, [(0, 0, 0)] * 3)
+    box = ((-4, -4, -4), (4, 4, 4))
+    out = oracle.render([ones, upper, ones], u0, beta_const(0.0), P, intr, 0.5, 4.0, 32, *box, t_eps=0.0)
+    acc = out["acc"].reshape(2, 2)
+    assert acc[0, 0] > 0.5 and acc[0, 1] > 0.5 and acc[1, 0] == 0 and acc[1, 1] == 0
+    out = oracle.render([ones, ones, right], u0, beta_const(0.0), P, intr, 0.5, 4.0, 32, *box, t_eps=0.0)
+    acc = out["acc"].reshape(2, 2)
+    assert acc[0, 1] > 0.5 and acc[1, 1] > 0.5 and acc[0, 0] == 0 and acc[1, 0] == 0
+
+
+# --------------------------------------------------------------------------
+# invariants on the seeded synthetic scenes
+# --------------------------------------------------------------------------
+
+@pytest.fixture(scope="module")
+def tiny_scene():
+    from paper_2204_02585_amd import scenes
+    return scenes.make_scene("tiny")
+
+
+def test_invariants_on_tiny_scene(tiny_scene):
+    """Eq. 1 with the exclusive prefix T_i: weights sum to 1 - T_stop
+    (telescoping), never exceed 1; colours are sigmoids so rgb lies in
+    [0, acc]; depth is a weighted mean of t in [near, far]; a stopped ray has
+    crossed the threshold."""
+    sc = tiny_scene
+    out = oracle.render_scene(sc)
+    N = sc.config.n_samples
+    T_end = np.exp(-out["tau_end"].astype(np.float64) * 2.0 ** -32)
+    assert np.all(np.abs(out["acc"] - (1.0 - T_end)) < N * 2.0 ** -32 + 1e-12)
+    assert np.all(out["acc"] <= 1.0 + 1e-12) and np.all(out["acc"] >= 0)
+    assert np.all(out["rgb"] >= 0) and np.all(out["rgb"] <= out["acc"][:, None] + 1e-12)
+    assert np.all(out["depth"] >= sc.near * out["acc"] - 1e-9)
+    assert np.all(out["depth"] <= sc.far * out["acc"] + 1e-9)
+    stopped = out["stop"] < N
+    assert np.all(out["tau_end"][stopped] > oracle.tau_eps_q(sc.config.t_eps))
+    assert np.all(out["n_occ"] <= out["n_inbox"]) and np.all(out["n_inbox"] <= out["stop"])
+    assert stopped.any() and (~stopped).any()
+
+
+def test_early_termination_changes_colour_by_at_most_eps(tiny_scene):
+    """Stopping once T < eps drops at most the remaining transmittance."""
+    sc = tiny_scene
+    a = oracle.render_scene(sc)
+    b = oracle.render_scene(sc, t_eps=0.0)
+    assert np.all(b["stop"] == sc.config.n_samples)
+    assert np.max(np.abs(a["rgb"] - b["rgb"])) <= 1e-4
+    assert np.max(np.abs(a["acc"] - b["acc"])) <= 1e-4
+
+
+def test_ray_subset_matches_full_render(tiny_scene):
+    sc = tiny_scene
+    full = oracle.render_scene(sc)
+    ids = np.array([0, 17, 2049, 4095, 1234], dtype=np.int64)
+    sub = oracle.render_scene(sc, ray_ids=ids)
+    assert np.array_equal(sub, full[ids])
