@@ -1,0 +1,168 @@
+#!/usr/bin/env python3
+"""Throughput of the cached SqueezeNeRF render path on one MI355X.
+
+One step = one sqn_render call over one batch of views (the whole hot path:
+ray generation, sample placement, cache gathers, beta . uvw colour and
+compositing).  Inputs (caches, poses, output buffers) are resident in HBM
+before the timed region.  Prints ONE JSON line.
+
+Default workload: 800x800 pixels, 192 samples per ray, position sub-caches
+k=256 with D=8 in fp16, 128x128 fp16 direction cache, 64 seeded blobs.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "Msamples/s and frames/s at 800x800x192 samples; achieved GB/s vs HBM peak"
+HBM_PEAK_GBS = 8000.0
+
+WORKLOAD_TEXT = {
+    "tiny": "64x64 image, 64 uniform samples/ray, k=64 D=8 fp32 caches, 32x32 fp32 direction cache, 16 blobs",
+    "paper": "800x800 image, 192 uniform samples/ray, k=256 D=8 fp16 caches, 128x128 fp16 direction cache, 64 blobs sigma_max 50",
+    "large": "800x800 image, 192 uniform samples/ray, k=1024 D=8 fp16 caches, 384x384 fp16 direction cache, 64 blobs sigma_max 200",
+    "batch": "100 spiral views of 800x800, 192 uniform samples/ray, k=256 D=8 fp16 caches, 128x128 fp16 direction cache",
+    "stress": "1920x1080 image, 384 stratified samples/ray, k=2048 D=16 fp16 caches, 512x512 fp16 direction cache, 256 blobs",
+}
+
+
+def algorithmic_bytes(cfg, n_rays, live_inbox, occupied):
+    """Bytes the method must move per launch: per ray the 4 direction-cache
+    texels (D values each), the pose row reads are broadcast and not
+    counted, 16 B of output (rgb + depth); per live in-box sample the three
+    sigma^j; per live occupied sample the three uvw records (3D values)."""
+    b = 2 if cfg.dtype == "f16" else 4
+    per_ray = 4 * cfg.D * b + 16
+    return n_rays * per_ray + live_inbox * 3 * b + occupied * 3 * 3 * cfg.D * b
+
+
+def cpu_baseline(scene, budget_s=12.0, max_frames=20):
+    """The CPU oracle as it stands, on whole frames of the same workload,
+    repeated until ~budget_s of wall time (at least one frame)."""
+    import oracle
+    threads = min(16, os.cpu_count() or 1)
+    cfg = scene.config
+    frames = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.render_scene(scene, poses=scene.poses[:1], n_threads=threads)
+        frames += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or frames >= max_frames:
+            break
+    samples = frames * cfg.width * cfg.height * cfg.n_samples
+    return {"value": samples / el / 1e6, "unit": "Msamples/s", "cores": threads, "kind": "oracle",
+            "sample": f"{frames} full {cfg.width}x{cfg.height}x{cfg.n_samples} frame(s) of view 0, "
+                      f"{el:.1f} s wall", "frames_per_s": frames / el}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="paper", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the render path has no cross-GPU step; "
+              "run it with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2204_02585_amd import binding, scenes
+
+    print(f"[bench] config={args.config} building scene", file=sys.stderr, flush=True)
+    scene = scenes.make_scene(args.config)
+    cfg = scene.config
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    caches = binding.caches_from_scene(scene, device=dev)
+    poses = torch.from_numpy(scene.poses).to(dev)
+    B = poses.shape[0]
+    rgb = torch.empty((B, cfg.height, cfg.width, 3), dtype=torch.float32, device=dev)
+    depth = torch.empty((B, cfg.height, cfg.width), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    N = cfg.n_samples
+
+    # untimed diagnostics pass: live / occupied sample counts for the byte model
+    _, _, st = caches.render_stats(poses, scene.intrinsics, scene.near, scene.far, N)
+    torch.cuda.synchronize()
+    st = st.cpu().numpy().view(np.uint32).reshape(-1, 4)
+    live_inbox = int(st[:, 1].astype(np.int64).sum())
+    occupied = int(st[:, 2].astype(np.int64).sum())
+    n_rays = B * cfg.width * cfg.height
+    bytes_alg = algorithmic_bytes(cfg, n_rays, live_inbox, occupied)
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        caches.render(poses, scene.intrinsics, scene.near, scene.far, N, rgb, depth, stream=stream)
+    torch.cuda.synchronize()
+
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        caches.render(poses, scene.intrinsics, scene.near, scene.far, N, rgb, depth, stream=stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = ev0.elapsed_time(ev1) / args.steps
+
+    nominal = cfg.nominal_samples
+    msps = nominal / (ms * 1e-3) / 1e6
+    fps = B / (ms * 1e-3)
+    gbs = bytes_alg / (ms * 1e-3) / 1e9
+
+    base = None
+    if not args.no_cpu_baseline:
+        print("[bench] CPU oracle baseline", file=sys.stderr, flush=True)
+        base = cpu_baseline(scene, budget_s=args.cpu_budget)
+    caches.close()
+
+    out = {
+        "metric": METRIC,
+        "value": round(msps, 2),
+        "unit": "Msamples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded blob density, uniform uvw and beta; no trained caches)",
+        "config": {"workload": f"{cfg.name}: {WORKLOAD_TEXT[cfg.name]}",
+                   "views_per_step": B, "width": cfg.width, "height": cfg.height,
+                   "samples_per_ray": N, "n_p": cfg.n_p, "D": cfg.D, "cache_dtype": cfg.dtype,
+                   "direction_cache": [cfg.n_theta, cfg.n_phi], "t_eps": cfg.t_eps},
+        "frames_per_s": round(fps, 2),
+        "samples": {"nominal_per_step": nominal, "live_inbox_per_step": live_inbox,
+                    "occupied_per_step": occupied},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": int(bytes_alg),
+                     "kernel_ms_per_launch": round(ms, 5)},
+        "cpu_baseline": base,
+        "wall_s_timed": round(wall, 4),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

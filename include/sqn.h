@@ -1,0 +1,172 @@
+/*
+ * sqn.h -- C ABI of the MI355X (gfx950) cached SqueezeNeRF renderer.
+ *
+ * The library renders novel views from SqueezeNeRF caches (Wadhwani &
+ * Kojima, "SqueezeNeRF: Further factorized FastNeRF for memory-efficient
+ * inference", CVPR-W 2022).  For each pixel of each camera view it
+ *   1. casts the pinhole ray through the pixel centre (Sec. 3.1),
+ *   2. places N samples between the near and far planes (Sec. 3.1, 3.4),
+ *   3. looks up sigma^j and (u^j, v^j, w^j) in the three factorized position
+ *      sub-caches with nearest-neighbour lookup (Sec. 3.3, 3.4) and fuses
+ *      them by Eq. 4 (sigma = product, k = sum over the planes),
+ *   4. looks up beta in the direction cache with bilinear interpolation
+ *      (Sec. 3.4),
+ *   5. forms colour c = sigmoid(beta^T (u, v, w)) (Eq. 2, then a sigmoid),
+ *   6. composites colour and depth along the ray by Eq. 1, stopping once the
+ *      transmittance T_i falls below eps.
+ *
+ * Conventions (not fixed by the paper; chosen here and used throughout):
+ *   - pose: row-major 3x4 camera-to-world [R | c] in binary32; the camera
+ *     looks down its -z axis, +x is right, +y is up;
+ *   - pixel (u, v) is sampled at its centre (u + 1/2, v + 1/2); v = 0 is the
+ *     top row; outputs are row-major [B][H][W];
+ *   - the ray direction is d = R (a, b, -1) with a = (u + 1/2 - cx) / fx and
+ *     b = -(v + 1/2 - cy) / fy, not normalised, so the sample parameter t is
+ *     depth along the camera axis and near/far are planes;
+ *   - uniform samples sit at t_i = near + i (far - near) / N; stratified
+ *     samples at t_i = near + (i + xi_i) (far - near) / N with xi_i taken
+ *     from SplitMix64 (counter = ray id * N + i, ray id = (b H + v) W + u);
+ *   - delta_i = max(0, t_{i+1} - t_i) |d| with t_N = far;
+ *   - plane j in (xy, yz, zx) is indexed [first axis][second axis]; grid
+ *     nodes are vertex-aligned over the box (node 0 on bbox_min, node n_p-1
+ *     on bbox_max); nearest node = floor(g + 1/2) clamped, g = (p - bmin)
+ *     (n_p - 1) / (bmax - bmin); samples outside the box have sigma = 0;
+ *   - sigma = max(0, (sigma^xy sigma^yz) sigma^zx);
+ *   - direction cache: theta = polar angle from world +z on n_theta nodes
+ *     spanning [0, pi] (clamped), phi = atan2(d_y, d_x) on n_phi periodic
+ *     nodes at -pi + b 2 pi / n_phi;
+ *   - the optical depth before sample i is accumulated exactly in 64-bit
+ *     fixed point (units of 2^-32, per-sample term truncated and capped at
+ *     2^16); sample i is evaluated iff that sum is <= floor(-ln(eps) 2^32),
+ *     i.e. T_i >= eps; eps = 0 disables termination;
+ *   - no background colour; depth is sum_i w_i t_i (0 for empty rays).
+ * Ray positions, sample positions, grid indices and termination decisions
+ * are evaluated in IEEE binary32 with one rounding per operation and no
+ * fused multiply-add, so they are reproducible bit for bit on any IEEE
+ * implementation; colour, transmittance and the sums are binary32 with
+ * binary64 accumulation.
+ *
+ * Threading and streams: every call is asynchronous on the given HIP stream
+ * (NULL = the default stream) unless stated; a cache handle is read-only
+ * while rendering, so renders on several streams may share one handle.
+ * Device faults surface at the caller's next synchronisation.
+ */
+#ifndef SQN_H
+#define SQN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SQN_OK = 0,
+    SQN_ERR_INVALID_ARG = 1,    /* argument out of range, bad pointer or size  */
+    SQN_ERR_OUT_OF_MEMORY = 2,  /* device allocation failed                     */
+    SQN_ERR_DEVICE = 3,         /* a HIP call or kernel launch failed           */
+    SQN_ERR_UNSUPPORTED = 4     /* valid but not supported by this build        */
+} sqn_status;
+
+typedef enum { SQN_F32 = 0, SQN_F16 = 1 } sqn_dtype;
+
+/* Opaque, library-owned device copy of the caches. */
+typedef struct sqn_caches sqn_caches;
+
+/* Cache description (Sec. 3.3).  The paper stores sigma^j in fp32 and
+ * u^j, v^j, w^j and beta in fp16; each dtype is chosen independently. */
+typedef struct {
+    int32_t n_p;          /* position grid nodes per axis, 2..8192            */
+    int32_t D;            /* radiance components per colour channel, 1..32    */
+    int32_t n_theta;      /* direction grid, polar angle, >= 2                */
+    int32_t n_phi;        /* direction grid, azimuth, >= 2                    */
+    int32_t sigma_dtype;  /* sqn_dtype of the sigma^j planes                  */
+    int32_t uvw_dtype;    /* sqn_dtype of the u^j, v^j, w^j planes            */
+    int32_t beta_dtype;   /* sqn_dtype of the direction cache                 */
+    int32_t stratified;   /* 0: uniform samples, 1: one seeded offset per bin */
+    float bbox_min[3];    /* scene box spanned by the position grids          */
+    float bbox_max[3];    /* (bbox_min < bbox_max on every axis, finite)      */
+    float t_eps;          /* transmittance threshold in [0, 1]; 0 = no stop   */
+    int32_t reserved;     /* must be 0                                        */
+    uint64_t seed;        /* stratified-sampling seed                         */
+} sqn_cache_desc;
+
+/* Pinhole intrinsics in pixels, shared by every view of a call. */
+typedef struct {
+    float fx, fy, cx, cy;
+    int32_t width, height;
+} sqn_intrinsics;
+
+/* Copy the caches into library-owned device memory on the current device.
+ *   sigma_planes[j]: device pointer, [n_p][n_p] of sigma_dtype, planes in the
+ *                    order xy, yz, zx (Sec. 3.2), indexed [first][second];
+ *   uvw_planes[j]:   device pointer, [n_p][n_p][3D] of uvw_dtype, each texel
+ *                    u[0..D) then v[0..D) then w[0..D) (Eq. 3 outputs);
+ *   beta:            device pointer, [n_theta][n_phi][D] of beta_dtype;
+ *   stream:          hipStream_t the copies are ordered on; the call waits
+ *                    for them, so the caller may free its arrays on return.
+ * Values must be finite.  On success *out owns the copy (free it with
+ * sqn_destroy); on failure *out is NULL and nothing is leaked.
+ * Errors: SQN_ERR_INVALID_ARG (NULL pointer, range, a pointer that is not
+ * HIP device memory or whose allocation is smaller than the array),
+ * SQN_ERR_OUT_OF_MEMORY, SQN_ERR_DEVICE. */
+sqn_status sqn_create_caches(const sqn_cache_desc* desc,
+                             const void* const sigma_planes[3],
+                             const void* const uvw_planes[3],
+                             const void* beta,
+                             void* stream,
+                             sqn_caches** out);
+
+/* Render n_poses views (Sec. 3.4, Eq. 1).
+ *   poses:      device pointer, [n_poses][3][4] binary32 camera-to-world;
+ *   intrinsics: host pointer, read during the call only;
+ *   near_plane < far_plane, both finite; 1 <= n_samples <= 32768;
+ *   rgb_out:    device pointer, [n_poses][H][W][3] binary32, written;
+ *   depth_out:  device pointer, [n_poses][H][W] binary32, written; may be NULL;
+ *   stream:     hipStream_t the kernel is launched on.
+ * n_poses == 0 is a no-op.  Allocates nothing; returns before the kernel
+ * finishes.  The handle must belong to the current device.
+ * Errors: SQN_ERR_INVALID_ARG (as above; output or pose buffers that are
+ * not device allocations large enough; more than 2^31-1 rays),
+ * SQN_ERR_DEVICE (launch failure). */
+sqn_status sqn_render(const sqn_caches* caches,
+                      const float* poses, int32_t n_poses,
+                      const sqn_intrinsics* intrinsics,
+                      float near_plane, float far_plane, int32_t n_samples,
+                      float* rgb_out, float* depth_out,
+                      void* stream);
+
+/* sqn_render plus per-ray diagnostics for bit-exact checks:
+ *   ray_stats: device pointer, [n_poses][H][W][4] uint32, written with
+ *     { stop:    first sample index that is not evaluated (T_i < eps), or N;
+ *       n_inbox: evaluated samples inside the box;
+ *       n_occ:   evaluated samples inside the box with sigma > 0;
+ *       hash:    32-bit FNV-1a over the little-endian words (i, ix, iy, iz)
+ *                of the occupied samples in order of i }.
+ * rgb_out may be NULL here.  Slower than sqn_render. */
+sqn_status sqn_render_stats(const sqn_caches* caches,
+                            const float* poses, int32_t n_poses,
+                            const sqn_intrinsics* intrinsics,
+                            float near_plane, float far_plane, int32_t n_samples,
+                            float* rgb_out, float* depth_out,
+                            uint32_t* ray_stats,
+                            void* stream);
+
+/* Bytes of device memory the handle owns. */
+size_t sqn_cache_device_bytes(const sqn_caches* caches);
+
+/* Free the handle and its device memory; NULL is a no-op.  The caller must
+ * ensure no render using the handle is still running. */
+void sqn_destroy(sqn_caches* caches);
+
+/* Static description of a status code. */
+const char* sqn_status_string(sqn_status status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* sqn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SQN_H */

@@ -231,13 +231,16 @@ static void render_ray(const job_t* J, int64_t ray_id, oracle_ray* out)
             sigma = fmaxf(0.0f, prod);
         }
 
-        /* delta_i: distance to the next sample (the far plane after the last). */
+        /* delta_i: distance to the next sample (the far plane after the
+         * last).  A sample without density adds nothing to the optical depth. */
         float gap = fmaxf(0.0f, t_next - t);
         float delta = gap * dnorm;
-        float q = sigma * delta;
-        int64_t Q = (int64_t)(fminf(q, 65536.0f) * 4294967296.0f);
+        float q = 0.0f;
+        int64_t Q = 0;
 
         if (sigma > 0.0f) {
+            q = sigma * delta;
+            Q = (int64_t)(fminf(q, 65536.0f) * 4294967296.0f);
             n_occ++;
             hash = fnv1a_word(hash, (uint32_t)i);
             hash = fnv1a_word(hash, (uint32_t)ix);

@@ -1,0 +1,207 @@
+"""ctypes binding of libsqn.so (include/sqn.h) over torch device tensors.
+
+Argument marshalling only: every step of the render runs in the HIP
+library.  torch provides device memory and the current stream.  Importing
+this module loads libsqn.so and raises if it has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libsqn.so")
+
+SQN_OK, SQN_ERR_INVALID_ARG, SQN_ERR_OUT_OF_MEMORY, SQN_ERR_DEVICE, SQN_ERR_UNSUPPORTED = range(5)
+SQN_F32, SQN_F16 = 0, 1
+
+EXPORTS = ("sqn_create_caches", "sqn_render", "sqn_render_stats", "sqn_cache_device_bytes",
+           "sqn_destroy", "sqn_status_string", "sqn_last_error")
+
+
+class CacheDesc(ctypes.Structure):
+    _fields_ = [("n_p", ctypes.c_int32), ("D", ctypes.c_int32),
+                ("n_theta", ctypes.c_int32), ("n_phi", ctypes.c_int32),
+                ("sigma_dtype", ctypes.c_int32), ("uvw_dtype", ctypes.c_int32),
+                ("beta_dtype", ctypes.c_int32), ("stratified", ctypes.c_int32),
+                ("bbox_min", ctypes.c_float * 3), ("bbox_max", ctypes.c_float * 3),
+                ("t_eps", ctypes.c_float), ("reserved", ctypes.c_int32),
+                ("seed", ctypes.c_uint64)]
+
+
+class Intrinsics(ctypes.Structure):
+    _fields_ = [("fx", ctypes.c_float), ("fy", ctypes.c_float),
+                ("cx", ctypes.c_float), ("cy", ctypes.c_float),
+                ("width", ctypes.c_int32), ("height", ctypes.c_int32)]
+
+
+class SqnError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"{status_string(status)}: {detail}")
+        self.status = status
+        self.detail = detail
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it first "
+                          "(python -m paper_2204_02585_amd.build)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
+    lib.sqn_create_caches.restype = ctypes.c_int
+    lib.sqn_create_caches.argtypes = [ctypes.POINTER(CacheDesc), ctypes.POINTER(vp),
+                                      ctypes.POINTER(vp), vp, vp, ctypes.POINTER(vp)]
+    lib.sqn_render.restype = ctypes.c_int
+    lib.sqn_render.argtypes = [vp, vp, i32, ctypes.POINTER(Intrinsics), f32, f32, i32, vp, vp, vp]
+    lib.sqn_render_stats.restype = ctypes.c_int
+    lib.sqn_render_stats.argtypes = [vp, vp, i32, ctypes.POINTER(Intrinsics), f32, f32, i32,
+                                     vp, vp, vp, vp]
+    lib.sqn_cache_device_bytes.restype = ctypes.c_size_t
+    lib.sqn_cache_device_bytes.argtypes = [vp]
+    lib.sqn_destroy.restype = None
+    lib.sqn_destroy.argtypes = [vp]
+    lib.sqn_status_string.restype = ctypes.c_char_p
+    lib.sqn_status_string.argtypes = [ctypes.c_int]
+    lib.sqn_last_error.restype = ctypes.c_char_p
+    lib.sqn_last_error.argtypes = []
+    return lib
+
+
+lib = _load()
+
+
+def status_string(status: int) -> str:
+    return lib.sqn_status_string(int(status)).decode()
+
+
+def last_error() -> str:
+    return lib.sqn_last_error().decode()
+
+
+def _check(status: int) -> None:
+    if status != SQN_OK:
+        raise SqnError(status, last_error())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float16:
+        return SQN_F16
+    if t.dtype == torch.float32:
+        return SQN_F32
+    raise TypeError(f"cache tensors must be float16 or float32, got {t.dtype}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _intrinsics(intr: dict) -> Intrinsics:
+    return Intrinsics(float(intr["fx"]), float(intr["fy"]), float(intr["cx"]), float(intr["cy"]),
+                      int(intr["width"]), int(intr["height"]))
+
+
+class Caches:
+    """Library-owned device copy of the SqueezeNeRF caches (sqn_create_caches)."""
+
+    def __init__(self, sigma: Sequence[torch.Tensor], uvw: Sequence[torch.Tensor],
+                 beta: torch.Tensor, bbox_min, bbox_max, t_eps: float = 1e-4,
+                 stratified: bool = False, seed: int = 0, stream=None):
+        self._h = ctypes.c_void_p(None)
+        sigma = [s.contiguous() for s in sigma]
+        uvw = [u.contiguous() for u in uvw]
+        beta = beta.contiguous()
+        n_p = sigma[0].shape[0]
+        D = uvw[0].shape[-1] // 3
+        desc = CacheDesc()
+        desc.n_p, desc.D = n_p, D
+        desc.n_theta, desc.n_phi = beta.shape[0], beta.shape[1]
+        desc.sigma_dtype, desc.uvw_dtype, desc.beta_dtype = (_dtype_code(sigma[0]), _dtype_code(uvw[0]),
+                                                             _dtype_code(beta))
+        desc.stratified = 1 if stratified else 0
+        for r in range(3):
+            desc.bbox_min[r] = bbox_min[r]
+            desc.bbox_max[r] = bbox_max[r]
+        desc.t_eps = t_eps
+        desc.reserved = 0
+        desc.seed = int(seed) & 0xFFFFFFFFFFFFFFFF
+        self.desc = desc
+        sp = (ctypes.c_void_p * 3)(*[s.data_ptr() for s in sigma])
+        up = (ctypes.c_void_p * 3)(*[u.data_ptr() for u in uvw])
+        _check(lib.sqn_create_caches(ctypes.byref(desc), sp, up, _ptr(beta), _stream(stream),
+                                     ctypes.byref(self._h)))
+
+    @property
+    def handle(self) -> ctypes.c_void_p:
+        if not self._h:
+            raise ValueError("caches have been destroyed")
+        return self._h
+
+    @property
+    def device_bytes(self) -> int:
+        return int(lib.sqn_cache_device_bytes(self.handle))
+
+    def close(self) -> None:
+        if self._h:
+            lib.sqn_destroy(self._h)
+            self._h = ctypes.c_void_p(None)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def render(self, poses: torch.Tensor, intrinsics: dict, near: float, far: float,
+               n_samples: int, rgb_out: Optional[torch.Tensor] = None,
+               depth_out: Optional[torch.Tensor] = None, with_depth: bool = True, stream=None):
+        """sqn_render; returns (rgb [B,H,W,3], depth [B,H,W] or None)."""
+        poses = poses.contiguous()
+        B = poses.shape[0]
+        H, W = int(intrinsics["height"]), int(intrinsics["width"])
+        if rgb_out is None:
+            rgb_out = torch.empty((B, H, W, 3), dtype=torch.float32, device=poses.device)
+        if depth_out is None and with_depth:
+            depth_out = torch.empty((B, H, W), dtype=torch.float32, device=poses.device)
+        intr = _intrinsics(intrinsics)
+        _check(lib.sqn_render(self.handle, _ptr(poses), B, ctypes.byref(intr), float(near),
+                              float(far), int(n_samples), _ptr(rgb_out), _ptr(depth_out),
+                              _stream(stream)))
+        return rgb_out, depth_out
+
+    def render_stats(self, poses: torch.Tensor, intrinsics: dict, near: float, far: float,
+                     n_samples: int, stream=None):
+        """sqn_render_stats; returns (rgb, depth, stats [B,H,W,4] int32 view of
+        {stop, n_inbox, n_occ, hash})."""
+        poses = poses.contiguous()
+        B = poses.shape[0]
+        H, W = int(intrinsics["height"]), int(intrinsics["width"])
+        rgb = torch.empty((B, H, W, 3), dtype=torch.float32, device=poses.device)
+        depth = torch.empty((B, H, W), dtype=torch.float32, device=poses.device)
+        stats = torch.empty((B, H, W, 4), dtype=torch.int32, device=poses.device)
+        intr = _intrinsics(intrinsics)
+        _check(lib.sqn_render_stats(self.handle, _ptr(poses), B, ctypes.byref(intr), float(near),
+                                    float(far), int(n_samples), _ptr(rgb), _ptr(depth),
+                                    _ptr(stats), _stream(stream)))
+        return rgb, depth, stats
+
+
+def caches_from_scene(scene, device="cuda", t_eps=None, stratified=None, stream=None) -> Caches:
+    """Upload a scene's host arrays (see scenes.Scene) and create the caches."""
+    cfg = scene.config
+    sig = [torch.from_numpy(a).to(device) for a in scene.sigma]
+    uvw = [torch.from_numpy(a).to(device) for a in scene.uvw]
+    beta = torch.from_numpy(scene.beta).to(device)
+    caches = Caches(sig, uvw, beta, scene.bbox_min, scene.bbox_max,
+                    t_eps=cfg.t_eps if t_eps is None else t_eps,
+                    stratified=cfg.stratified if stratified is None else stratified,
+                    seed=scene.seed, stream=stream)
+    return caches

@@ -1,0 +1,371 @@
+// C ABI of the cached SqueezeNeRF renderer: argument validation, the
+// library-owned device copy of the caches, and the render launches.
+// Declarations and contracts: include/sqn.h.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <limits>
+#include <string>
+
+#include "sqn_internal.h"
+
+struct sqn_caches {
+    sqn_cache_desc desc;
+    int device;
+    void* block;             // one hipMalloc holding every plane
+    size_t bytes;
+    const void* sigma[3];
+    const void* uvw[3];
+    const void* beta;
+    float scale[3];          // (n_p - 1) / (bmax - bmin), binary32
+    int64_t tau_eps;         // floor(-ln(eps) 2^32)
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+sqn_status fail(sqn_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+
+sqn_status fail(sqn_status s, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
+size_t dtype_size(int32_t dt) { return dt == SQN_F16 ? 2 : 4; }
+
+bool valid_dtype(int32_t dt) { return dt == SQN_F32 || dt == SQN_F16; }
+
+// The pointer must lie in a HIP device allocation with at least `bytes`
+// bytes from it to the end of the allocation.
+sqn_status check_device_range(const void* p, size_t bytes, const char* what)
+{
+    if (!p)
+        return fail(SQN_ERR_INVALID_ARG, "%s is NULL", what);
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    hipError_t e = hipMemGetAddressRange(&base, &size, const_cast<void*>(p));
+    if (e != hipSuccess || base == nullptr) {
+        (void)hipGetLastError();
+        return fail(SQN_ERR_INVALID_ARG, "%s (%p) is not HIP device memory", what, p);
+    }
+    const uintptr_t lo = reinterpret_cast<uintptr_t>(base);
+    const uintptr_t q = reinterpret_cast<uintptr_t>(p);
+    if (q < lo || q - lo > size || size - (q - lo) < bytes)
+        return fail(SQN_ERR_INVALID_ARG,
+                    "%s (%p) needs %zu bytes but its allocation ends %zu bytes after it", what,
+                    p, bytes, size - (q - lo));
+    return SQN_OK;
+}
+
+int64_t tau_threshold(float eps)
+{
+    if (!(eps > 0.0f))
+        return std::numeric_limits<int64_t>::max();
+    const double x = -log(static_cast<double>(eps)) * 4294967296.0;
+    if (x <= 0.0)
+        return 0;
+    return static_cast<int64_t>(floor(x));
+}
+
+sqn_status validate_desc(const sqn_cache_desc* d)
+{
+    if (!d)
+        return fail(SQN_ERR_INVALID_ARG, "desc is NULL");
+    if (d->n_p < 2 || d->n_p > 8192)
+        return fail(SQN_ERR_INVALID_ARG, "n_p = %d outside [2, 8192]", d->n_p);
+    if (d->D < 1 || d->D > 32)
+        return fail(SQN_ERR_INVALID_ARG, "D = %d outside [1, 32]", d->D);
+    if (d->n_theta < 2 || d->n_phi < 2 || d->n_theta > 65536 || d->n_phi > 65536
+        || static_cast<int64_t>(d->n_theta) * d->n_phi * d->D > (int64_t{1} << 31))
+        return fail(SQN_ERR_INVALID_ARG, "direction grid %d x %d x %d out of range", d->n_theta,
+                    d->n_phi, d->D);
+    if (!valid_dtype(d->sigma_dtype) || !valid_dtype(d->uvw_dtype) || !valid_dtype(d->beta_dtype))
+        return fail(SQN_ERR_INVALID_ARG, "dtype must be SQN_F32 or SQN_F16");
+    if (d->stratified != 0 && d->stratified != 1)
+        return fail(SQN_ERR_INVALID_ARG, "stratified must be 0 or 1");
+    if (d->reserved != 0)
+        return fail(SQN_ERR_INVALID_ARG, "reserved must be 0");
+    for (int r = 0; r < 3; ++r)
+        if (!isfinite(d->bbox_min[r]) || !isfinite(d->bbox_max[r]) || !(d->bbox_min[r] < d->bbox_max[r])
+            || !isfinite(d->bbox_max[r] - d->bbox_min[r]))
+            return fail(SQN_ERR_INVALID_ARG, "bbox axis %d is empty or not finite", r);
+    if (!(d->t_eps >= 0.0f && d->t_eps <= 1.0f))
+        return fail(SQN_ERR_INVALID_ARG, "t_eps = %g outside [0, 1]", static_cast<double>(d->t_eps));
+    // every uvw plane is addressed with 32-bit element offsets
+    const uint64_t texels = static_cast<uint64_t>(d->n_p) * d->n_p;
+    if (texels * 3u * d->D >= (uint64_t{1} << 32))
+        return fail(SQN_ERR_UNSUPPORTED, "n_p^2 * 3D = %llu exceeds 2^32 elements per plane",
+                    static_cast<unsigned long long>(texels * 3u * d->D));
+    return SQN_OK;
+}
+
+sqn_status validate_render(const sqn_caches* h, const float* poses, int32_t n_poses,
+                           const sqn_intrinsics* in, float near_plane, float far_plane,
+                           int32_t n_samples, const float* rgb, const float* depth,
+                           const uint32_t* stats, bool need_rgb, int* device)
+{
+    if (!h)
+        return fail(SQN_ERR_INVALID_ARG, "caches is NULL");
+    if (!in)
+        return fail(SQN_ERR_INVALID_ARG, "intrinsics is NULL");
+    if (n_poses < 0)
+        return fail(SQN_ERR_INVALID_ARG, "n_poses = %d is negative", n_poses);
+    if (in->width < 1 || in->height < 1)
+        return fail(SQN_ERR_INVALID_ARG, "image %d x %d is empty", in->width, in->height);
+    if (!isfinite(in->fx) || !isfinite(in->fy) || in->fx == 0.0f || in->fy == 0.0f
+        || !isfinite(in->cx) || !isfinite(in->cy))
+        return fail(SQN_ERR_INVALID_ARG, "intrinsics must be finite with fx, fy != 0");
+    if (!isfinite(near_plane) || !isfinite(far_plane) || !(near_plane < far_plane))
+        return fail(SQN_ERR_INVALID_ARG, "need finite near < far (got %g, %g)",
+                    static_cast<double>(near_plane), static_cast<double>(far_plane));
+    if (n_samples < 1 || n_samples > 32768)
+        return fail(SQN_ERR_INVALID_ARG, "n_samples = %d outside [1, 32768]", n_samples);
+    const int64_t rays = static_cast<int64_t>(n_poses) * in->width * in->height;
+    if (rays > std::numeric_limits<int32_t>::max())
+        return fail(SQN_ERR_INVALID_ARG, "%lld rays exceed 2^31 - 1", static_cast<long long>(rays));
+    if (hipGetDevice(device) != hipSuccess)
+        return fail(SQN_ERR_DEVICE, "hipGetDevice failed");
+    if (*device != h->device)
+        return fail(SQN_ERR_INVALID_ARG, "caches live on device %d, current device is %d",
+                    h->device, *device);
+    if (n_poses == 0)
+        return SQN_OK;
+    const size_t nr = static_cast<size_t>(rays);
+    sqn_status s = check_device_range(poses, static_cast<size_t>(n_poses) * 12 * sizeof(float), "poses");
+    if (s != SQN_OK)
+        return s;
+    if (need_rgb || rgb) {
+        s = check_device_range(rgb, nr * 3 * sizeof(float), "rgb_out");
+        if (s != SQN_OK)
+            return s;
+    }
+    if (depth) {
+        s = check_device_range(depth, nr * sizeof(float), "depth_out");
+        if (s != SQN_OK)
+            return s;
+    }
+    if (stats) {
+        s = check_device_range(stats, nr * 4 * sizeof(uint32_t), "ray_stats");
+        if (s != SQN_OK)
+            return s;
+    }
+    return SQN_OK;
+}
+
+sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_poses,
+                         const sqn_intrinsics* in, float near_plane, float far_plane,
+                         int32_t n_samples, float* rgb, float* depth, uint32_t* stats,
+                         void* stream)
+{
+    int device = -1;
+    const bool with_stats = stats != nullptr;
+    sqn_status s = validate_render(h, poses, n_poses, in, near_plane, far_plane, n_samples, rgb,
+                                   depth, stats, !with_stats, &device);
+    if (s != SQN_OK)
+        return s;
+    if (n_poses == 0)
+        return SQN_OK;
+
+    sqn::RenderParams p;
+    memset(&p, 0, sizeof(p));
+    for (int j = 0; j < 3; ++j) {
+        p.sigma[j] = h->sigma[j];
+        p.uvw[j] = h->uvw[j];
+    }
+    p.beta = h->beta;
+    p.poses = poses;
+    p.rgb = rgb;
+    p.depth = depth;
+    p.stats = stats;
+    p.fx = in->fx;
+    p.fy = in->fy;
+    p.cx = in->cx;
+    p.cy = in->cy;
+    p.width = in->width;
+    p.height = in->height;
+    p.n_views = n_poses;
+    p.near_t = near_plane;
+    p.far_t = far_plane;
+    p.n_samples = n_samples;
+    p.dt = (far_plane - near_plane) / static_cast<float>(n_samples);
+    p.stratified = h->desc.stratified;
+    for (int r = 0; r < 3; ++r) {
+        p.bmin[r] = h->desc.bbox_min[r];
+        p.bmax[r] = h->desc.bbox_max[r];
+        p.scale[r] = h->scale[r];
+    }
+    p.n_p = h->desc.n_p;
+    p.D = h->desc.D;
+    p.n_theta = h->desc.n_theta;
+    p.n_phi = h->desc.n_phi;
+    p.beta_f16 = h->desc.beta_dtype == SQN_F16;
+    p.rec_bytes = static_cast<uint32_t>(3 * h->desc.D * dtype_size(h->desc.uvw_dtype));
+    p.tau_eps = h->tau_eps;
+    p.seed = h->desc.seed;
+    p.tiles_x = (in->width + sqn::kTileW - 1) / sqn::kTileW;
+    p.tiles_y = (in->height + sqn::kTileH - 1) / sqn::kTileH;
+    const int64_t groups = static_cast<int64_t>(p.tiles_x) * p.tiles_y * n_poses;
+    if (groups > std::numeric_limits<int32_t>::max())
+        return fail(SQN_ERR_INVALID_ARG, "too many workgroups (%lld)", static_cast<long long>(groups));
+    p.n_groups = static_cast<int32_t>(groups);
+
+    hipError_t e = sqn::launch_render(p, h->desc.sigma_dtype, h->desc.uvw_dtype, with_stats,
+                                      static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return fail(SQN_ERR_DEVICE, "render launch failed: %s", hipGetErrorString(e));
+    return SQN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sqn_status sqn_create_caches(const sqn_cache_desc* desc, const void* const sigma_planes[3],
+                             const void* const uvw_planes[3], const void* beta, void* stream,
+                             sqn_caches** out)
+{
+    if (!out)
+        return fail(SQN_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    sqn_status s = validate_desc(desc);
+    if (s != SQN_OK)
+        return s;
+    if (!sigma_planes || !uvw_planes)
+        return fail(SQN_ERR_INVALID_ARG, "plane pointer array is NULL");
+
+    const size_t texels = static_cast<size_t>(desc->n_p) * desc->n_p;
+    const size_t sigma_bytes = texels * dtype_size(desc->sigma_dtype);
+    const size_t uvw_bytes = texels * 3 * desc->D * dtype_size(desc->uvw_dtype);
+    const size_t beta_bytes = static_cast<size_t>(desc->n_theta) * desc->n_phi * desc->D
+                              * dtype_size(desc->beta_dtype);
+    static const char* names_s[3] = {"sigma_planes[0] (xy)", "sigma_planes[1] (yz)", "sigma_planes[2] (zx)"};
+    static const char* names_u[3] = {"uvw_planes[0] (xy)", "uvw_planes[1] (yz)", "uvw_planes[2] (zx)"};
+    for (int j = 0; j < 3; ++j) {
+        if ((s = check_device_range(sigma_planes[j], sigma_bytes, names_s[j])) != SQN_OK)
+            return s;
+        if ((s = check_device_range(uvw_planes[j], uvw_bytes, names_u[j])) != SQN_OK)
+            return s;
+    }
+    if ((s = check_device_range(beta, beta_bytes, "beta")) != SQN_OK)
+        return s;
+
+    auto align = [](size_t x) { return (x + 255) & ~size_t{255}; };
+    size_t off_sigma[3], off_uvw[3], off_beta, total = 0;
+    for (int j = 0; j < 3; ++j) {
+        off_sigma[j] = total;
+        total += align(sigma_bytes);
+    }
+    for (int j = 0; j < 3; ++j) {
+        off_uvw[j] = total;
+        total += align(uvw_bytes);
+    }
+    off_beta = total;
+    total += align(beta_bytes);
+
+    sqn_caches* h = static_cast<sqn_caches*>(calloc(1, sizeof(sqn_caches)));
+    if (!h)
+        return fail(SQN_ERR_OUT_OF_MEMORY, "host allocation failed");
+    h->desc = *desc;
+    if (hipGetDevice(&h->device) != hipSuccess) {
+        free(h);
+        return fail(SQN_ERR_DEVICE, "hipGetDevice failed");
+    }
+    if (getenv("SQN_TEST_FAIL_ALLOC") != nullptr) {
+        free(h);
+        return fail(SQN_ERR_OUT_OF_MEMORY, "device allocation of %zu bytes refused (SQN_TEST_FAIL_ALLOC)", total);
+    }
+    hipError_t e = hipMalloc(&h->block, total);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        free(h);
+        return fail(SQN_ERR_OUT_OF_MEMORY, "hipMalloc(%zu) failed: %s", total, hipGetErrorString(e));
+    }
+    h->bytes = total;
+    char* base = static_cast<char*>(h->block);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    for (int j = 0; j < 3 && e == hipSuccess; ++j) {
+        h->sigma[j] = base + off_sigma[j];
+        h->uvw[j] = base + off_uvw[j];
+        e = hipMemcpyAsync(base + off_sigma[j], sigma_planes[j], sigma_bytes, hipMemcpyDeviceToDevice, st);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(base + off_uvw[j], uvw_planes[j], uvw_bytes, hipMemcpyDeviceToDevice, st);
+    }
+    h->beta = base + off_beta;
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(base + off_beta, beta, beta_bytes, hipMemcpyDeviceToDevice, st);
+    if (e == hipSuccess)
+        e = hipStreamSynchronize(st);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        (void)hipFree(h->block);
+        free(h);
+        return fail(SQN_ERR_DEVICE, "cache upload failed: %s", hipGetErrorString(e));
+    }
+    for (int r = 0; r < 3; ++r)
+        h->scale[r] = static_cast<float>(desc->n_p - 1) / (desc->bbox_max[r] - desc->bbox_min[r]);
+    h->tau_eps = tau_threshold(desc->t_eps);
+    *out = h;
+    g_last_error.clear();
+    return SQN_OK;
+}
+
+sqn_status sqn_render(const sqn_caches* caches, const float* poses, int32_t n_poses,
+                      const sqn_intrinsics* intrinsics, float near_plane, float far_plane,
+                      int32_t n_samples, float* rgb_out, float* depth_out, void* stream)
+{
+    return render_common(caches, poses, n_poses, intrinsics, near_plane, far_plane, n_samples,
+                         rgb_out, depth_out, nullptr, stream);
+}
+
+sqn_status sqn_render_stats(const sqn_caches* caches, const float* poses, int32_t n_poses,
+                            const sqn_intrinsics* intrinsics, float near_plane, float far_plane,
+                            int32_t n_samples, float* rgb_out, float* depth_out,
+                            uint32_t* ray_stats, void* stream)
+{
+    if (!ray_stats)
+        return fail(SQN_ERR_INVALID_ARG, "ray_stats is NULL");
+    return render_common(caches, poses, n_poses, intrinsics, near_plane, far_plane, n_samples,
+                         rgb_out, depth_out, ray_stats, stream);
+}
+
+size_t sqn_cache_device_bytes(const sqn_caches* caches) { return caches ? caches->bytes : 0; }
+
+void sqn_destroy(sqn_caches* caches)
+{
+    if (!caches)
+        return;
+    if (caches->block)
+        (void)hipFree(caches->block);
+    free(caches);
+}
+
+const char* sqn_status_string(sqn_status status)
+{
+    switch (status) {
+    case SQN_OK:
+        return "success";
+    case SQN_ERR_INVALID_ARG:
+        return "invalid argument";
+    case SQN_ERR_OUT_OF_MEMORY:
+        return "out of device memory";
+    case SQN_ERR_DEVICE:
+        return "HIP device error";
+    case SQN_ERR_UNSUPPORTED:
+        return "unsupported configuration";
+    }
+    return "unknown status";
+}
+
+const char* sqn_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

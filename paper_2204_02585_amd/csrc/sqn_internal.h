@@ -1,0 +1,54 @@
+// Internal types shared by the C ABI layer (api.hip) and the render kernels
+// (render.hip).  Not part of the public interface.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sqn.h"
+
+namespace sqn {
+
+// Everything one render launch reads, passed by value as the kernel argument.
+struct RenderParams {
+    // caches (library-owned device memory)
+    const void* sigma[3];     // [n_p][n_p], planes xy, yz, zx
+    const void* uvw[3];       // [n_p][n_p][3D] records
+    const void* beta;         // [n_theta][n_phi][D]
+    // camera batch and outputs (caller-owned device memory)
+    const float* poses;       // [B][3][4]
+    float* rgb;               // [B][H][W][3] or null (stats launches)
+    float* depth;             // [B][H][W] or null
+    uint32_t* stats;          // [B][H][W][4] or null
+    // camera
+    float fx, fy, cx, cy;
+    int32_t width, height, n_views;
+    // sampling
+    float near_t, far_t, dt;  // dt = (far - near) / N in binary32
+    int32_t n_samples;
+    int32_t stratified;       // 1: seeded offset inside each bin
+    // grid
+    float bmin[3], bmax[3];
+    float scale[3];           // (n_p - 1) / (bmax - bmin) in binary32
+    int32_t n_p, D, n_theta, n_phi;
+    int32_t beta_f16;
+    uint32_t rec_bytes;       // bytes of one uvw record (3D values)
+    int64_t tau_eps;          // floor(-ln(eps) 2^32), INT64_MAX for eps = 0
+    uint64_t seed;
+    // launch geometry
+    int32_t tiles_x, tiles_y; // workgroup tiles per view
+    int32_t n_groups;         // workgroups in the grid
+};
+
+// Launch one render over all views on `stream`; `stats` selects the variant
+// that writes per-ray diagnostics.  Shapes have been validated by the
+// caller.  Returns the launch status.
+hipError_t launch_render(const RenderParams& p, int sigma_dtype, int uvw_dtype,
+                         bool stats, hipStream_t stream);
+
+// Workgroup geometry used by launch_render (pixels per workgroup tile).
+constexpr int kTileW = 16;
+constexpr int kTileH = 16;
+constexpr int kBlockThreads = 256;
+
+}  // namespace sqn

@@ -1,0 +1,80 @@
+"""Host-side checks of the C-ABI library that need no GPU: it loads, it
+exports every function include/sqn.h declares, and argument validation that
+happens before any device call returns the documented statuses."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "sqn.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(sqn_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2204_02585_amd import binding
+    return binding
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for required in ("sqn_create_caches", "sqn_render", "sqn_destroy"):
+        assert required in names
+
+
+def test_library_exports_every_declared_function(lib):
+    raw = ctypes.CDLL(lib.LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(raw, name), name
+    assert set(_declared_functions()) == set(lib.EXPORTS)
+
+
+def test_status_strings(lib):
+    assert lib.status_string(lib.SQN_OK) == "success"
+    assert "invalid" in lib.status_string(lib.SQN_ERR_INVALID_ARG)
+    assert lib.status_string(99) == "unknown status"
+
+
+def test_validation_before_device_calls(lib):
+    """NULL descriptors, out-of-range sizes and NULL handles are rejected by
+    host code alone."""
+    vp = ctypes.c_void_p
+    out = vp()
+    planes = (vp * 3)()
+    assert lib.lib.sqn_create_caches(None, planes, planes, None, None, ctypes.byref(out)) \
+        == lib.SQN_ERR_INVALID_ARG
+    assert "desc" in lib.last_error()
+    desc = lib.CacheDesc()
+    desc.n_p, desc.D, desc.n_theta, desc.n_phi = 1, 8, 4, 4
+    for r in range(3):
+        desc.bbox_min[r], desc.bbox_max[r] = -1.0, 1.0
+    assert lib.lib.sqn_create_caches(ctypes.byref(desc), planes, planes, None, None,
+                                     ctypes.byref(out)) == lib.SQN_ERR_INVALID_ARG
+    assert "n_p" in lib.last_error()
+    desc.n_p = 64
+    desc.D = 0
+    assert lib.lib.sqn_create_caches(ctypes.byref(desc), planes, planes, None, None,
+                                     ctypes.byref(out)) == lib.SQN_ERR_INVALID_ARG
+    desc.D = 8
+    desc.sigma_dtype = 7
+    assert lib.lib.sqn_create_caches(ctypes.byref(desc), planes, planes, None, None,
+                                     ctypes.byref(out)) == lib.SQN_ERR_INVALID_ARG
+    desc.sigma_dtype = 0
+    desc.t_eps = float("nan")
+    assert lib.lib.sqn_create_caches(ctypes.byref(desc), planes, planes, None, None,
+                                     ctypes.byref(out)) == lib.SQN_ERR_INVALID_ARG
+    desc.t_eps = 1e-4
+    desc.n_p, desc.D = 8192, 32
+    assert lib.lib.sqn_create_caches(ctypes.byref(desc), planes, planes, None, None,
+                                     ctypes.byref(out)) == lib.SQN_ERR_UNSUPPORTED
+    intr = lib.Intrinsics(1.0, 1.0, 0.5, 0.5, 1, 1)
+    assert lib.lib.sqn_render(None, None, 1, ctypes.byref(intr), 2.0, 6.0, 8, None, None,
+                              None) == lib.SQN_ERR_INVALID_ARG
+    assert lib.lib.sqn_cache_device_bytes(None) == 0
+    lib.lib.sqn_destroy(None)

@@ -1,0 +1,284 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Full frames at the small size; at the full workload sizes, sampled rays the
+oracle renders one by one plus properties over the whole frame.  Values
+within the stated tolerance, per-ray stop index, sample counts and the hash
+of the occupied (i, ix, iy, iz) sequence bit-exact.
+"""
+import dataclasses
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2204_02585_amd import scenes
+from tests import parity_util as pu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a visible GPU"
+    from paper_2204_02585_amd import binding  # noqa: F401  (fails loudly without libsqn.so)
+
+
+# ---------------------------------------------------------------- small sizes
+
+@pytest.mark.parametrize("t_eps", [1e-4, 0.0])
+def test_tiny_full_frame(t_eps):
+    sc = scenes.make_scene("tiny")
+    gpu = pu.gpu_render(sc, t_eps=t_eps)
+    ref = oracle.render_scene(sc, t_eps=t_eps)
+    ids = np.arange(ref.size)
+    pu.compare(gpu, ref, ids, pu.scene_atol(sc), f"tiny eps={t_eps}")
+    assert (ref["n_occ"] > 0).sum() > 100
+
+
+def _small(name, **kw):
+    """A small variant of a named workload (same cache shape family)."""
+    cfg = dataclasses.replace(scenes.CONFIGS[name], **kw)
+    return scenes.make_scene(cfg)
+
+
+@pytest.mark.parametrize("W,H", [(37, 23), (1, 1), (16, 16), (17, 1), (1, 33)])
+def test_ragged_and_degenerate_image_sizes(W, H):
+    sc = _small("tiny", width=W, height=H, focal=1.25 * max(W, H))
+    gpu = pu.gpu_render(sc)
+    ref = oracle.render_scene(sc)
+    pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), f"{W}x{H}")
+
+
+@pytest.mark.parametrize("N", [1, 2, 7, 384, 4096])
+def test_sample_counts(N):
+    sc = _small("tiny", width=24, height=20, n_samples=N)
+    gpu = pu.gpu_render(sc)
+    ref = oracle.render_scene(sc)
+    pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), f"N={N}")
+
+
+@pytest.mark.parametrize("D", [1, 3, 8, 16, 32])
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+def test_component_counts_and_dtypes(D, dtype):
+    """Specialised (D = 8, 16) and generic kernels, both storage types."""
+    sc = _small("tiny", width=40, height=40, D=D, dtype=dtype, n_p=48, n_theta=9, n_phi=12)
+    gpu = pu.gpu_render(sc)
+    ref = oracle.render_scene(sc)
+    pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), f"D={D} {dtype}")
+
+
+def test_paper_precision_mix():
+    """sigma^j in fp32, u^j v^j w^j and beta in fp16 (Sec. 3.3)."""
+    sc = _small("tiny", width=48, height=48)
+    sc.uvw = [a.astype(np.float16) for a in sc.uvw]
+    sc.beta = sc.beta.astype(np.float16)
+    gpu = pu.gpu_render(sc)
+    ref = oracle.render_scene(sc)
+    pu.compare(gpu, ref, np.arange(ref.size), 1e-5, "sigma f32 / uvw f16")
+
+
+def test_stratified_small():
+    sc = _small("tiny", width=32, height=32, stratified=True)
+    gpu = pu.gpu_render(sc)
+    ref = oracle.render_scene(sc)
+    pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), "stratified")
+
+
+def test_multi_view_batch_small():
+    sc = _small("tiny", width=20, height=12)
+    poses = scenes.spiral_poses(7)
+    gpu = pu.gpu_render(sc, poses=poses)
+    ref = oracle.render_scene(sc, poses=poses)
+    pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), "7 views")
+
+
+def test_camera_inside_box_and_axis_rays():
+    """Rays that start inside the box, run along box faces or have zero
+    direction components (the clip's exact special case)."""
+    sc = _small("tiny", width=9, height=9, focal=4.0)
+    P = np.zeros((4, 3, 4), np.float32)
+    # looking along +y from inside the box
+    P[0, :, 0], P[0, :, 1], P[0, :, 2], P[0, :, 3] = (1, 0, 0), (0, 0, 1), (0, -1, 0), (0.1, -0.2, 0.3)
+    # on the x = -1.5 face, looking along +y
+    P[1, :, 0], P[1, :, 1], P[1, :, 2], P[1, :, 3] = (1, 0, 0), (0, 0, 1), (0, -1, 0), (-1.5, -4, 0.0)
+    # on an edge (x = 1.5, z = -1.5), looking along +y
+    P[2, :, 0], P[2, :, 1], P[2, :, 2], P[2, :, 3] = (1, 0, 0), (0, 0, 1), (0, -1, 0), (1.5, -4, -1.5)
+    # looking straight down -z from above
+    P[3, :, 0], P[3, :, 1], P[3, :, 2], P[3, :, 3] = (1, 0, 0), (0, 1, 0), (0, 0, 1), (0.2, 0.1, 4)
+    gpu = pu.gpu_render(sc, poses=P)
+    ref = oracle.render_scene(sc, poses=P)
+    pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), "inside/axis")
+    assert ref["n_inbox"].sum() > 0
+
+
+def test_dense_scene_terminates():
+    """sigma_max 2000: most rays stop within a few samples."""
+    sc = _small("tiny", width=48, height=48, sigma_max=2000.0)
+    gpu = pu.gpu_render(sc)
+    ref = oracle.render_scene(sc)
+    pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), "dense")
+    assert (ref["stop"] < sc.config.n_samples).mean() > 0.1
+
+
+def test_empty_batch_is_noop():
+    import torch
+    from paper_2204_02585_amd import binding
+    sc = scenes.make_scene("tiny")
+    caches = binding.caches_from_scene(sc)
+    try:
+        P = torch.zeros((0, 3, 4), device="cuda")
+        rgb, depth = caches.render(P, sc.intrinsics, sc.near, sc.far, 64)
+        torch.cuda.synchronize()
+        assert rgb.shape == (0, 64, 64, 3)
+    finally:
+        caches.close()
+
+
+# ------------------------------------------------------- full workload sizes
+
+@pytest.mark.parametrize("name,n_random", [("paper", 40000), ("large", 40000)])
+def test_full_size_single_view(name, n_random):
+    sc = scenes.make_scene(name)
+    cfg = sc.config
+    gpu = pu.gpu_render(sc)
+    ids = pu.sample_ray_ids(1, cfg.height, cfg.width, n_random, seed=cfg.number)
+    ref = oracle.render_scene(sc, ray_ids=ids)
+    pu.compare(gpu, ref, ids, pu.scene_atol(sc), name)
+    rgb, depth, st = gpu
+    # whole-frame properties
+    assert np.all(rgb >= 0) and np.all(rgb <= 1.0 + 1e-6)
+    assert np.all(depth >= 0) and np.all(depth <= sc.far + 1e-4)
+    assert np.all(st[:, 0] <= cfg.n_samples) and np.all(st[:, 2] <= st[:, 1])
+
+
+def test_full_size_batch():
+    sc = scenes.make_scene("batch")
+    cfg = sc.config
+    gpu = pu.gpu_render(sc)
+    ids = pu.sample_ray_ids(cfg.n_poses, cfg.height, cfg.width, 30000, seed=4)
+    ref = oracle.render_scene(sc, ray_ids=ids)
+    pu.compare(gpu, ref, ids, pu.scene_atol(sc), "batch")
+
+
+def test_full_size_stress():
+    sc = scenes.make_scene("stress")
+    cfg = sc.config
+    gpu = pu.gpu_render(sc)
+    ids = pu.sample_ray_ids(1, cfg.height, cfg.width, 20000, seed=5)
+    ref = oracle.render_scene(sc, ray_ids=ids)
+    pu.compare(gpu, ref, ids, pu.scene_atol(sc), "stress")
+
+
+# ------------------------------------------------------------ C-ABI errors
+
+def test_abi_rejects_bad_arguments():
+    import ctypes
+    import torch
+    from paper_2204_02585_amd import binding
+    sc = scenes.make_scene("tiny")
+    caches = binding.caches_from_scene(sc)
+    lib = binding.lib
+    pose_buf = pu.DeviceBuffer(48)
+    small = pu.DeviceBuffer(4096)
+    try:
+        P = torch.from_numpy(sc.poses).cuda()
+        intr = binding.Intrinsics(80.0, 80.0, 32.0, 32.0, 64, 64)
+        rgb = torch.empty((1, 64, 64, 3), device="cuda")
+        h = caches.handle
+        vp = ctypes.c_void_p
+
+        def render(poses=vp(P.data_ptr()), n=1, intr_=ctypes.byref(intr), near=2.0, far=6.0,
+                   N=64, out=vp(rgb.data_ptr()), depth=None):
+            return lib.sqn_render(h, poses, n, intr_, near, far, N, out, depth, None)
+
+        assert render() == binding.SQN_OK
+        assert render(near=6.0, far=2.0) == binding.SQN_ERR_INVALID_ARG
+        assert render(near=2.0, far=2.0) == binding.SQN_ERR_INVALID_ARG
+        assert render(far=math.nan) == binding.SQN_ERR_INVALID_ARG
+        assert render(N=0) == binding.SQN_ERR_INVALID_ARG
+        assert render(N=40000) == binding.SQN_ERR_INVALID_ARG
+        assert render(n=-1) == binding.SQN_ERR_INVALID_ARG
+        # 100000 poses need 4.8 MB; this allocation holds one (allocation
+        # granularity may round it up, but not to megabytes)
+        assert render(poses=pose_buf.ptr, n=100000) == binding.SQN_ERR_INVALID_ARG
+        assert "poses" in binding.last_error()
+        # a 2048x2048 rgb image needs 48 MiB
+        big = binding.Intrinsics(80.0, 80.0, 32.0, 32.0, 2048, 2048)
+        assert render(intr_=ctypes.byref(big), out=small.ptr) == binding.SQN_ERR_INVALID_ARG
+        assert "rgb_out" in binding.last_error()
+        assert render(out=None) == binding.SQN_ERR_INVALID_ARG
+        host = (ctypes.c_float * 12)()
+        assert render(poses=ctypes.cast(host, vp)) == binding.SQN_ERR_INVALID_ARG
+        assert render(intr_=None) == binding.SQN_ERR_INVALID_ARG
+        bad = binding.Intrinsics(0.0, 80.0, 32.0, 32.0, 64, 64)
+        assert render(intr_=ctypes.byref(bad)) == binding.SQN_ERR_INVALID_ARG
+        empty = binding.Intrinsics(80.0, 80.0, 32.0, 32.0, 0, 64)
+        assert render(intr_=ctypes.byref(empty)) == binding.SQN_ERR_INVALID_ARG
+        assert lib.sqn_render(None, vp(P.data_ptr()), 1, ctypes.byref(intr), 2.0, 6.0, 64,
+                              vp(rgb.data_ptr()), None, None) == binding.SQN_ERR_INVALID_ARG
+        assert lib.sqn_render_stats(h, vp(P.data_ptr()), 1, ctypes.byref(intr), 2.0, 6.0, 64,
+                                    vp(rgb.data_ptr()), None, None, None) == binding.SQN_ERR_INVALID_ARG
+        torch.cuda.synchronize()
+    finally:
+        caches.close()
+        pose_buf.free()
+        small.free()
+    lib.sqn_destroy(None)
+
+
+def test_create_rejects_bad_descriptions_and_undersized_arrays():
+    import ctypes
+    import torch
+    from paper_2204_02585_amd import binding
+    sc = scenes.make_scene("tiny")
+    sig = [torch.from_numpy(a).cuda() for a in sc.sigma]
+    uvw = [torch.from_numpy(a).cuda() for a in sc.uvw]
+    beta = torch.from_numpy(sc.beta).cuda()
+    with pytest.raises(binding.SqnError) as e:
+        binding.Caches(sig, uvw, beta, (1, 1, 1), (-1, -1, -1))
+    assert e.value.status == binding.SQN_ERR_INVALID_ARG
+    with pytest.raises(binding.SqnError) as e:
+        binding.Caches(sig, uvw, beta, sc.bbox_min, sc.bbox_max, t_eps=2.0)
+    assert e.value.status == binding.SQN_ERR_INVALID_ARG
+    # n_p = 2048 needs 16 MiB sigma planes and 384 MiB uvw planes; the
+    # arrays given are far smaller
+    short = pu.DeviceBuffer(4096)
+    try:
+        desc = binding.CacheDesc()
+        desc.n_p, desc.D, desc.n_theta, desc.n_phi = 2048, 8, 32, 32
+        for r in range(3):
+            desc.bbox_min[r], desc.bbox_max[r] = -1.5, 1.5
+        desc.t_eps = 1e-4
+        vp = ctypes.c_void_p
+        sp = (vp * 3)(*[s.data_ptr() for s in sig])
+        up = (vp * 3)(uvw[0].data_ptr(), short.ptr.value, uvw[2].data_ptr())
+        out = vp()
+        rc = binding.lib.sqn_create_caches(ctypes.byref(desc), sp, up, vp(beta.data_ptr()), None,
+                                           ctypes.byref(out))
+        assert rc == binding.SQN_ERR_INVALID_ARG and not out
+        assert "sigma_planes[0]" in binding.last_error()
+        desc.D = 33
+        up = (vp * 3)(*[u.data_ptr() for u in uvw])
+        assert binding.lib.sqn_create_caches(ctypes.byref(desc), sp, up, vp(beta.data_ptr()), None,
+                                             ctypes.byref(out)) == binding.SQN_ERR_INVALID_ARG
+    finally:
+        short.free()
+
+
+def test_create_out_of_memory_hook(monkeypatch):
+    import torch
+    from paper_2204_02585_amd import binding
+    sc = scenes.make_scene("tiny")
+    monkeypatch.setenv("SQN_TEST_FAIL_ALLOC", "1")
+    free0 = torch.cuda.mem_get_info()[0]
+    with pytest.raises(binding.SqnError) as e:
+        binding.caches_from_scene(sc)
+    assert e.value.status == binding.SQN_ERR_OUT_OF_MEMORY
+    monkeypatch.delenv("SQN_TEST_FAIL_ALLOC")
+    c = binding.caches_from_scene(sc)
+    assert c.device_bytes >= sc.cache_nbytes()
+    c.close()
+    torch.cuda.synchronize()
+    assert torch.cuda.mem_get_info()[0] >= free0 - (64 << 20)
