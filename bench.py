@@ -45,7 +45,7 @@ def algorithmic_bytes(cfg, n_rays, live_inbox, occupied):
     return n_rays * per_ray + live_inbox * 3 * b + occupied * 3 * 3 * cfg.D * b
 
 
-def cpu_baseline(scene, budget_s=12.0, max_frames=20):
+def cpu_baseline(scene, budget_s=12.0, max_frames=40):
     """The CPU oracle as it stands, on whole frames of the same workload,
     repeated until ~budget_s of wall time (at least one frame)."""
     import oracle
@@ -71,8 +71,13 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="paper", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--lanes", type=int, default=0,
+                    help="lanes of a wavefront per ray (1, 2, 4); 0 = the library's choice")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed region, copy 1 GiB device-to-device 3 times (a kernel "
+                         "of known traffic for scaling hardware byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -89,6 +94,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     caches = binding.caches_from_scene(scene, device=dev)
+    caches.set_lanes_per_ray(args.lanes)
     poses = torch.from_numpy(scene.poses).to(dev)
     B = poses.shape[0]
     rgb = torch.empty((B, cfg.height, cfg.width, 3), dtype=torch.float32, device=dev)
@@ -128,6 +134,14 @@ def main():
     fps = B / (ms * 1e-3)
     gbs = bytes_alg / (ms * 1e-3) / 1e9
 
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     base = None
     if not args.no_cpu_baseline:
         print("[bench] CPU oracle baseline", file=sys.stderr, flush=True)
@@ -150,7 +164,8 @@ def main():
         "config": {"workload": f"{cfg.name}: {WORKLOAD_TEXT[cfg.name]}",
                    "views_per_step": B, "width": cfg.width, "height": cfg.height,
                    "samples_per_ray": N, "n_p": cfg.n_p, "D": cfg.D, "cache_dtype": cfg.dtype,
-                   "direction_cache": [cfg.n_theta, cfg.n_phi], "t_eps": cfg.t_eps},
+                   "direction_cache": [cfg.n_theta, cfg.n_phi], "t_eps": cfg.t_eps,
+                   "lanes_per_ray": args.lanes or "auto"},
         "frames_per_s": round(fps, 2),
         "samples": {"nominal_per_step": nominal, "live_inbox_per_step": live_inbox,
                     "occupied_per_step": occupied},

@@ -153,6 +153,15 @@ sqn_status sqn_render_stats(const sqn_caches* caches,
                             uint32_t* ray_stats,
                             void* stream);
 
+/* Launch shape of later renders with this handle: how many lanes of a
+ * wavefront share one ray (1, 2 or 4; each lane takes every L-th sample of a
+ * chunk of L consecutive samples), or 0 (the default) to choose from the
+ * number of rays of each call.  Sample, index and termination decisions are
+ * identical for every choice; colour and depth agree up to the rounding of
+ * their sums.  Not thread-safe against concurrent renders with the handle.
+ * Errors: SQN_ERR_INVALID_ARG. */
+sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes);
+
 /* Bytes of device memory the handle owns. */
 size_t sqn_cache_device_bytes(const sqn_caches* caches);
 

@@ -18,8 +18,8 @@ LIB_PATH = os.path.join(_PKG, "libsqn.so")
 SQN_OK, SQN_ERR_INVALID_ARG, SQN_ERR_OUT_OF_MEMORY, SQN_ERR_DEVICE, SQN_ERR_UNSUPPORTED = range(5)
 SQN_F32, SQN_F16 = 0, 1
 
-EXPORTS = ("sqn_create_caches", "sqn_render", "sqn_render_stats", "sqn_cache_device_bytes",
-           "sqn_destroy", "sqn_status_string", "sqn_last_error")
+EXPORTS = ("sqn_create_caches", "sqn_render", "sqn_render_stats", "sqn_set_lanes_per_ray",
+           "sqn_cache_device_bytes", "sqn_destroy", "sqn_status_string", "sqn_last_error")
 
 
 class CacheDesc(ctypes.Structure):
@@ -59,6 +59,8 @@ def _load() -> ctypes.CDLL:
     lib.sqn_render_stats.restype = ctypes.c_int
     lib.sqn_render_stats.argtypes = [vp, vp, i32, ctypes.POINTER(Intrinsics), f32, f32, i32,
                                      vp, vp, vp, vp]
+    lib.sqn_set_lanes_per_ray.restype = ctypes.c_int
+    lib.sqn_set_lanes_per_ray.argtypes = [vp, i32]
     lib.sqn_cache_device_bytes.restype = ctypes.c_size_t
     lib.sqn_cache_device_bytes.argtypes = [vp]
     lib.sqn_destroy.restype = None
@@ -148,6 +150,10 @@ class Caches:
     @property
     def device_bytes(self) -> int:
         return int(lib.sqn_cache_device_bytes(self.handle))
+
+    def set_lanes_per_ray(self, lanes: int) -> None:
+        """1, 2 or 4 lanes of a wavefront per ray, or 0 to choose per call."""
+        _check(lib.sqn_set_lanes_per_ray(self.handle, int(lanes)))
 
     def close(self) -> None:
         if self._h:

@@ -23,6 +23,9 @@ HIPCC_FLAGS = [
     "-ffp-contract=off",
     "-fhip-fp32-correctly-rounded-divide-sqrt",
     "-fno-gpu-flush-denormals-to-zero",
+    # the SLP vectorizer packs the six box comparisons into bit vectors;
+    # scalar compares into lane masks are cheaper
+    "-fno-slp-vectorize",
     # packed binary32 VALU forms are kept out of generated code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall",

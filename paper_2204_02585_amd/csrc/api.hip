@@ -22,6 +22,7 @@ struct sqn_caches {
     const void* beta;
     float scale[3];          // (n_p - 1) / (bmax - bmin), binary32
     int64_t tau_eps;         // floor(-ln(eps) 2^32)
+    int32_t lanes;           // lanes per ray, 0 = chosen per call
 };
 
 namespace {
@@ -101,11 +102,12 @@ sqn_status validate_desc(const sqn_cache_desc* d)
             return fail(SQN_ERR_INVALID_ARG, "bbox axis %d is empty or not finite", r);
     if (!(d->t_eps >= 0.0f && d->t_eps <= 1.0f))
         return fail(SQN_ERR_INVALID_ARG, "t_eps = %g outside [0, 1]", static_cast<double>(d->t_eps));
-    // every uvw plane is addressed with 32-bit element offsets
+    // every plane is addressed with 32-bit byte offsets
     const uint64_t texels = static_cast<uint64_t>(d->n_p) * d->n_p;
-    if (texels * 3u * d->D >= (uint64_t{1} << 32))
-        return fail(SQN_ERR_UNSUPPORTED, "n_p^2 * 3D = %llu exceeds 2^32 elements per plane",
-                    static_cast<unsigned long long>(texels * 3u * d->D));
+    const uint64_t uvw_plane = texels * 3u * d->D * dtype_size(d->uvw_dtype);
+    if (uvw_plane >= (uint64_t{1} << 32))
+        return fail(SQN_ERR_UNSUPPORTED, "a uvw plane of %llu bytes exceeds 2^32 bytes",
+                    static_cast<unsigned long long>(uvw_plane));
     return SQN_OK;
 }
 
@@ -162,6 +164,16 @@ sqn_status validate_render(const sqn_caches* h, const float* poses, int32_t n_po
     return SQN_OK;
 }
 
+// Lanes per ray for a call of `rays` rays.  One lane per ray does the least
+// work per sample, but a wave lives as long as its longest ray and 256 CUs x
+// 4 SIMDs x 8 waves hold only 8192 waves: below about 2^20 rays (one 800x800
+// view is 10^4 waves) the last waves run nearly alone, and four lanes per ray
+// (4x the waves, each 4x shorter) finish sooner despite the cross-lane scan.
+int choose_lanes(int64_t rays)
+{
+    return rays < (int64_t{1} << 20) ? 4 : 1;
+}
+
 sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_poses,
                          const sqn_intrinsics* in, float near_plane, float far_plane,
                          int32_t n_samples, float* rgb, float* depth, uint32_t* stats,
@@ -212,8 +224,11 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
     p.rec_bytes = static_cast<uint32_t>(3 * h->desc.D * dtype_size(h->desc.uvw_dtype));
     p.tau_eps = h->tau_eps;
     p.seed = h->desc.seed;
-    p.tiles_x = (in->width + sqn::kTileW - 1) / sqn::kTileW;
-    p.tiles_y = (in->height + sqn::kTileH - 1) / sqn::kTileH;
+    p.inv_dt = 1.0f / p.dt;
+    p.lanes = h->lanes != 0 ? h->lanes : choose_lanes(static_cast<int64_t>(n_poses) * in->width * in->height);
+    const int tw = sqn::kTileW(p.lanes), th = sqn::kTileH(p.lanes);
+    p.tiles_x = (in->width + tw - 1) / tw;
+    p.tiles_y = (in->height + th - 1) / th;
     const int64_t groups = static_cast<int64_t>(p.tiles_x) * p.tiles_y * n_poses;
     if (groups > std::numeric_limits<int32_t>::max())
         return fail(SQN_ERR_INVALID_ARG, "too many workgroups (%lld)", static_cast<long long>(groups));
@@ -336,6 +351,16 @@ sqn_status sqn_render_stats(const sqn_caches* caches, const float* poses, int32_
         return fail(SQN_ERR_INVALID_ARG, "ray_stats is NULL");
     return render_common(caches, poses, n_poses, intrinsics, near_plane, far_plane, n_samples,
                          rgb_out, depth_out, ray_stats, stream);
+}
+
+sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes)
+{
+    if (!caches)
+        return fail(SQN_ERR_INVALID_ARG, "caches is NULL");
+    if (lanes != 0 && lanes != 1 && lanes != 2 && lanes != 4)
+        return fail(SQN_ERR_INVALID_ARG, "lanes per ray must be 0, 1, 2 or 4 (got %d)", lanes);
+    caches->lanes = lanes;
+    return SQN_OK;
 }
 
 size_t sqn_cache_device_bytes(const sqn_caches* caches) { return caches ? caches->bytes : 0; }

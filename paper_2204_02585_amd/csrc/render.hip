@@ -1,25 +1,27 @@
 // Render kernels of the cached SqueezeNeRF path for gfx950 (CDNA4).
 //
-// One lane renders one pixel ray; a wave64 covers an 8x8 pixel tile, a
-// 256-thread workgroup a 16x16 tile.  Neighbouring rays of a tile sit a
-// fraction of a texel apart at equal sample index (samples are equal-depth
-// planes), so the nearest-node gathers of a wave hit a handful of texels and
-// cache lines: the wave-wide gather is what coalesces, not the sample axis.
+// Work layout.  L consecutive lanes of a wave64 (L = 1, 2 or 4) share one
+// pixel ray and walk its samples in chunks of L consecutive samples, one per
+// lane; a wave holds 64/L rays laid out as a compact pixel tile.  Rays of a
+// tile sit a fraction of a texel apart at equal sample index (samples lie on
+// equal-depth planes), so the nearest-node gathers of one wave-wide load hit
+// a few texels and cache lines.  L > 1 multiplies the number of waves of a
+// frame (a single 800x800 view is only 10^4 waves at L = 1) at the price of a
+// short cross-lane scan per chunk.
 //
-// Per ray: pinhole ray (Sec. 3.1), a conservative clip of the sample range
-// to the scene box (samples outside it have sigma = 0 and contribute
-// nothing), the bilinear direction lookup of beta (Sec. 3.4) once, then a
-// march over the samples: nearest-node gather of the three sigma^j and
-// their product (Eq. 4), the fixed-point optical depth and termination test
-// (Eq. 1 with T_i >= eps), and only for live samples with sigma > 0 the
-// three uvw records, their sum (Eq. 4), the inner product with beta (Eq. 2),
-// a sigmoid and the Eq. 1 weights.
+// Per ray: pinhole ray (Sec. 3.1); a conservative clip of the sample range to
+// the scene box (samples outside it have sigma = 0 and add nothing); the
+// bilinear direction lookup of beta (Sec. 3.4).  Per sample: nearest-node
+// gathers of the three sigma^j and their product (Eq. 4); the 2^-32
+// fixed-point optical depth increment, scanned exactly across the L lanes;
+// the termination test T_i >= eps (Eq. 1); and only for live samples with
+// sigma > 0 the three uvw records, beta^T (sum of the planar uvw) (Eq. 4 and
+// Eq. 2), a sigmoid and the Eq. 1 weight.
 //
-// This file must be compiled with -ffp-contract=off and correctly rounded
-// binary32 division and square root: the ray, sample, index and termination
-// arithmetic is specified as one rounding per written operation.  Fused
-// multiply-adds are requested explicitly (fmaf) where only the value path
-// uses them.
+// Compile with -ffp-contract=off and correctly rounded binary32 division and
+// square root: ray, sample, grid-index and termination arithmetic is
+// specified as one rounding per written operation.  The value path requests
+// fused multiply-adds explicitly.
 #include <math.h>
 
 #include "sqn_internal.h"
@@ -28,37 +30,162 @@ namespace sqn {
 namespace {
 
 constexpr double kPi = 3.14159265358979323846;
+constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ float widen(float x) { return x; }
 __device__ __forceinline__ float widen(_Float16 x) { return static_cast<float>(x); }
 
+// Element at byte offset `off` (32-bit) from a uniform base pointer.
 template <typename T>
-__device__ __forceinline__ float load_value(const void* base, uint32_t idx)
+__device__ __forceinline__ T load_at(const void* base, uint32_t off)
 {
-    return widen(static_cast<const T*>(base)[idx]);
+    return *reinterpret_cast<const T*>(static_cast<const char*>(base) + off);
+}
+
+// ---------------------------------------------------------------------------
+// lanes of one ray: L consecutive lanes inside a quad, exchanged with DPP
+// quad permutations (the group is always entirely active or inactive)
+
+constexpr int qperm(int a, int b, int c, int d) { return a | (b << 2) | (c << 4) | (d << 6); }
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp32(uint32_t x)
+{
+    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), CTRL, 0xf, 0xf, true));
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp64(uint64_t x)
+{
+    const uint32_t lo = dpp32<CTRL>(static_cast<uint32_t>(x));
+    const uint32_t hi = dpp32<CTRL>(static_cast<uint32_t>(x >> 32));
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dppf(float x)
+{
+    return __uint_as_float(dpp32<CTRL>(__float_as_uint(x)));
+}
+
+// value of lane s + 1 of the group (the last lane reads itself)
+template <int L>
+__device__ __forceinline__ float grp_next(float x)
+{
+    if constexpr (L == 2)
+        return dppf<qperm(1, 1, 3, 3)>(x);
+    else if constexpr (L == 4)
+        return dppf<qperm(1, 2, 3, 3)>(x);
+    else
+        return x;
+}
+
+// value of lane 0 of the group
+template <int L>
+__device__ __forceinline__ float grp_first(float x)
+{
+    if constexpr (L == 2)
+        return dppf<qperm(0, 0, 2, 2)>(x);
+    else if constexpr (L == 4)
+        return dppf<qperm(0, 0, 0, 0)>(x);
+    else
+        return x;
+}
+
+// Exclusive prefix sum of q over the group (lane order) and the group total.
+template <int L>
+__device__ __forceinline__ void grp_scan(uint64_t q, int s, uint64_t& excl, uint64_t& total)
+{
+    if constexpr (L == 1) {
+        excl = 0;
+        total = q;
+    } else if constexpr (L == 2) {
+        const uint64_t other = dpp64<qperm(1, 0, 3, 2)>(q);
+        excl = s ? other : 0;
+        total = q + other;
+    } else {
+        uint64_t y = q;
+        const uint64_t y1 = dpp64<qperm(0, 0, 1, 2)>(y);
+        y += (s >= 1) ? y1 : 0;
+        const uint64_t y2 = dpp64<qperm(0, 0, 0, 1)>(y);
+        y += (s >= 2) ? y2 : 0;
+        excl = y - q;
+        total = dpp64<qperm(3, 3, 3, 3)>(y);
+    }
+}
+
+template <int L>
+__device__ __forceinline__ float grp_sum(float x)
+{
+    if constexpr (L >= 2)
+        x += dppf<qperm(1, 0, 3, 2)>(x);
+    if constexpr (L == 4)
+        x += dppf<qperm(2, 3, 0, 1)>(x);
+    return x;
+}
+
+template <int L>
+__device__ __forceinline__ double grp_sum(double x)
+{
+    if constexpr (L >= 2)
+        x += __shfl_xor(x, 1, L);
+    if constexpr (L == 4)
+        x += __shfl_xor(x, 2, L);
+    return x;
+}
+
+template <int L>
+__device__ __forceinline__ int32_t grp_max(int32_t x)
+{
+    if constexpr (L >= 2)
+        x = max(x, static_cast<int32_t>(dpp32<qperm(1, 0, 3, 2)>(static_cast<uint32_t>(x))));
+    if constexpr (L == 4)
+        x = max(x, static_cast<int32_t>(dpp32<qperm(2, 3, 0, 1)>(static_cast<uint32_t>(x))));
+    return x;
+}
+
+template <int L>
+__device__ __forceinline__ uint32_t grp_add(uint32_t x)
+{
+    if constexpr (L >= 2)
+        x += dpp32<qperm(1, 0, 3, 2)>(x);
+    if constexpr (L == 4)
+        x += dpp32<qperm(2, 3, 0, 1)>(x);
+    return x;
 }
 
 // ---------------------------------------------------------------------------
 // exact path (binary32, one rounding per operation)
 
-// Nearest vertex-aligned node along one axis; ties round up.
-__device__ __forceinline__ int32_t nearest_node(float p, float lo, float scale, int32_t n_p)
+// (int)floor(x) in one instruction; exact for every x this code passes
+// (finite, |x| < 2^31).
+__device__ __forceinline__ int32_t floor_to_int(float x)
 {
-    float g = (p - lo) * scale;
-    int32_t i = static_cast<int32_t>(floorf(g + 0.5f));
-    return min(i, n_p - 1);
+    int32_t r;
+    asm("v_cvt_flr_i32_f32 %0, %1" : "=v"(r) : "v"(x));
+    return r;
 }
 
-// trunc(min(q, 2^16) * 2^32) for q >= 0, without a float->int64 conversion:
-// the integer part and the (exactly representable) fraction convert
-// separately.
-__device__ __forceinline__ int64_t fixed_q(float q)
+// Nearest vertex-aligned node along one axis; ties round up:
+// floor(g + 1/2) with g = (p - lo) scale.  For a sample inside the box
+// 1/2 <= g + 1/2 < n_p, so clamping g + 1/2 to [0, n_p - 1] before the floor
+// gives min(floor(g + 1/2), n_p - 1) there and a valid index everywhere.
+__device__ __forceinline__ uint32_t nearest_node(float p, float lo, float scale, float hi_node)
 {
-    float qc = fminf(q, 65536.0f);
-    float hi = floorf(qc);
-    float frac = qc - hi;
-    uint32_t lo = static_cast<uint32_t>(frac * 4294967296.0f);
-    return static_cast<int64_t>((static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | lo);
+    const float g = (p - lo) * scale;
+    const float h = g + 0.5f;
+    return static_cast<uint32_t>(floor_to_int(__builtin_amdgcn_fmed3f(h, 0.0f, hi_node)));
+}
+
+// trunc(min(q, 2^16) * 2^32) for q >= 0: the integer part and the (exactly
+// representable) fraction convert separately.
+__device__ __forceinline__ uint64_t fixed_q(float q)
+{
+    const float qc = fminf(q, 65536.0f);
+    const float hi = floorf(qc);
+    const float frac = qc - hi;
+    const uint32_t lo = static_cast<uint32_t>(frac * 4294967296.0f);
+    return (static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | lo;
 }
 
 // SplitMix64 (Steele, Lea & Flood 2014): output number `counter` (0-based)
@@ -78,53 +205,49 @@ __device__ __forceinline__ float sample_t(const RenderParams& P, bool stratified
 {
     float x = static_cast<float>(i);
     if (stratified) {
-        uint64_t h = splitmix64(P.seed, ray_key + static_cast<uint64_t>(i));
-        float xi = static_cast<float>(static_cast<uint32_t>(h >> 40)) * 0x1p-24f;
+        const uint64_t h = splitmix64(P.seed, ray_key + static_cast<uint64_t>(i));
+        const float xi = static_cast<float>(static_cast<uint32_t>(h >> 40)) * 0x1p-24f;
         x = x + xi;
     }
-    float xd = x * P.dt;
+    const float xd = x * P.dt;
     return P.near_t + xd;
 }
 
 // Conservative sample-index range [i0, i1] of the scene box: every sample
-// outside it fails the exact in-box test.  The face crossings are computed
-// in binary64 and widened by far more than the binary32 evaluation of
-// o + t d can misplace them, then widened by two more samples.
-__device__ inline void clip_to_box(const RenderParams& P, const float o[3], const float d[3],
-                                   int32_t& i0, int32_t& i1)
+// outside it fails the exact in-box test.  Face crossings are widened by
+// 1e-5 relative (far beyond the few-ulp misplacement of the binary32
+// position o + t d and of this estimate), then by two samples.  An axis with
+// a (nearly) zero direction component constrains nothing here unless the
+// component is exactly zero, where p = o holds exactly.
+__device__ __forceinline__ void clip_to_box(const RenderParams& P, const float o[3],
+                                            const float d[3], int32_t& i0, int32_t& i1)
 {
-    double lo = -INFINITY, hi = INFINITY;
+    float lo = -INFINITY, hi = INFINITY;
+    bool empty = false;
+#pragma unroll
     for (int r = 0; r < 3; ++r) {
         if (d[r] == 0.0f) {
-            // p_r = o_r exactly for every t
-            if (!(o[r] >= P.bmin[r] && o[r] <= P.bmax[r])) {
-                i0 = 1;
-                i1 = 0;
-                return;
-            }
-            continue;
+            empty = empty || !(o[r] >= P.bmin[r] && o[r] <= P.bmax[r]);
+        } else if (fabsf(d[r]) > 1e-20f) {
+            const float inv = __builtin_amdgcn_rcpf(d[r]);
+            const float ta = (P.bmin[r] - o[r]) * inv;
+            const float tb = (P.bmax[r] - o[r]) * inv;
+            const float tmin = fminf(ta, tb), tmax = fmaxf(ta, tb);
+            const float bmag = fmaxf(fabsf(P.bmin[r]), fabsf(P.bmax[r]));
+            const float m = 1e-5f * (fmaxf(fabsf(tmin), fabsf(tmax)) + (fabsf(o[r]) + bmag) * fabsf(inv));
+            lo = fmaxf(lo, tmin - m);
+            hi = fminf(hi, tmax + m);
         }
-        const double dr = d[r], orr = o[r];
-        const double ta = (static_cast<double>(P.bmin[r]) - orr) / dr;
-        const double tb = (static_cast<double>(P.bmax[r]) - orr) / dr;
-        const double tmin = fmin(ta, tb), tmax = fmax(ta, tb);
-        const double bmag = fmax(fabs(static_cast<double>(P.bmin[r])),
-                                 fabs(static_cast<double>(P.bmax[r])));
-        const double m = 1e-5 * (fmax(fabs(tmin), fabs(tmax)) + (fabs(orr) + bmag) / fabs(dr));
-        lo = fmax(lo, tmin - m);
-        hi = fmin(hi, tmax + m);
     }
-    if (!(lo <= hi)) {
-        i0 = 1;
-        i1 = 0;
-        return;
+    const float n_last = static_cast<float>(P.n_samples - 1);
+    float f0 = floorf((lo - P.near_t) * P.inv_dt) - 2.0f;
+    float f1 = ceilf((hi - P.near_t) * P.inv_dt) + 2.0f;
+    f0 = fminf(fmaxf(f0, 0.0f), n_last + 1.0f);
+    f1 = fminf(fmaxf(f1, -1.0f), n_last);
+    if (empty || !(lo <= hi)) {
+        f0 = 1.0f;
+        f1 = 0.0f;
     }
-    const double n_last = static_cast<double>(P.n_samples - 1);
-    const double dt = P.dt;
-    double f0 = floor((lo - static_cast<double>(P.near_t)) / dt) - 2.0;
-    double f1 = ceil((hi - static_cast<double>(P.near_t)) / dt) + 2.0;
-    f0 = fmin(fmax(f0, 0.0), n_last + 1.0);
-    f1 = fmin(fmax(f1, -1.0), n_last);
     i0 = static_cast<int32_t>(f0);
     i1 = static_cast<int32_t>(f1);
 }
@@ -132,15 +255,33 @@ __device__ inline void clip_to_box(const RenderParams& P, const float o[3], cons
 // ---------------------------------------------------------------------------
 // value path
 
-// Bilinear lookup of beta (Sec. 3.4), once per ray, in binary64: theta is
-// the polar angle from +z on a clamped grid over [0, pi], phi = atan2 on a
-// periodic grid starting at -pi.
-template <int DC>
-__device__ inline void lookup_beta(const RenderParams& P, const float d[3], float* beta)
+// Bilinear lookup of beta (Sec. 3.4), once per ray.  The angles and grid
+// coordinates are computed in binary64 (theta = polar angle from +z on a
+// clamped grid over [0, pi]; phi = atan2 on a periodic grid from -pi); with
+// L >= 2 the even lanes of the group evaluate theta and the odd lanes phi,
+// and each lane weights a share of the four corner texels before a group
+// sum.
+template <int DC, int L>
+__device__ __forceinline__ void lookup_beta(const RenderParams& P, const float d[3], int s,
+                                            float* beta_lds)
 {
     const double dx = d[0], dy = d[1], dz = d[2];
-    const double theta = atan2(sqrt(dx * dx + dy * dy), dz);
-    const double phi = atan2(dy, dx);
+    double theta, phi;
+    if constexpr (L == 1) {
+        theta = atan2(sqrt(dx * dx + dy * dy), dz);
+        phi = atan2(dy, dx);
+    } else {
+        const bool odd = (s & 1) != 0;
+        const double ang = atan2(odd ? dy : sqrt(dx * dx + dy * dy), odd ? dx : dz);
+        const uint32_t lo = static_cast<uint32_t>(__double_as_longlong(ang));
+        const uint32_t hi = static_cast<uint32_t>(static_cast<uint64_t>(__double_as_longlong(ang)) >> 32);
+        // even lane -> theta, odd lane -> phi, exchanged within each pair
+        const uint32_t lo_o = dpp32<qperm(1, 0, 3, 2)>(lo);
+        const uint32_t hi_o = dpp32<qperm(1, 0, 3, 2)>(hi);
+        const double other = __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi_o) << 32) | lo_o));
+        theta = odd ? other : ang;
+        phi = odd ? ang : other;
+    }
 
     const double gt = theta * static_cast<double>(P.n_theta - 1) / kPi;
     int32_t a0 = static_cast<int32_t>(floor(gt));
@@ -155,86 +296,96 @@ __device__ inline void lookup_beta(const RenderParams& P, const float d[3], floa
     const int32_t b1 = (b0 + 1 == P.n_phi) ? 0 : b0 + 1;
 
     const int32_t D = DC > 0 ? DC : P.D;
-    const uint32_t r0 = static_cast<uint32_t>(a0 * P.n_phi);
-    const uint32_t r1 = static_cast<uint32_t>((a0 + 1) * P.n_phi);
-    const uint32_t i00 = (r0 + b0) * D, i01 = (r0 + b1) * D;
-    const uint32_t i10 = (r1 + b0) * D, i11 = (r1 + b1) * D;
-    const double w00 = (1.0 - ft) * (1.0 - fp), w01 = (1.0 - ft) * fp;
-    const double w10 = ft * (1.0 - fp), w11 = ft * fp;
+    const uint32_t row0 = static_cast<uint32_t>(a0 * P.n_phi);
+    const uint32_t row1 = static_cast<uint32_t>((a0 + 1) * P.n_phi);
+    // corners c = 0..3: (a0,b0) (a0,b1) (a0+1,b0) (a0+1,b1)
+    const uint32_t texel[4] = {row0 + b0, row0 + b1, row1 + b0, row1 + b1};
+    const float wgt[4] = {static_cast<float>((1.0 - ft) * (1.0 - fp)), static_cast<float>((1.0 - ft) * fp),
+                          static_cast<float>(ft * (1.0 - fp)), static_cast<float>(ft * fp)};
+    const uint32_t esz = P.beta_f16 ? 2u : 4u;
+    auto component = [&](int k) {
+        float acc = 0.0f;
 #pragma unroll
-    for (int32_t k = 0; k < (DC > 0 ? DC : 32); ++k) {
-        if (DC == 0 && k >= D)
-            break;
-        double v00, v01, v10, v11;
-        if (P.beta_f16) {
-            v00 = load_value<_Float16>(P.beta, i00 + k);
-            v01 = load_value<_Float16>(P.beta, i01 + k);
-            v10 = load_value<_Float16>(P.beta, i10 + k);
-            v11 = load_value<_Float16>(P.beta, i11 + k);
-        } else {
-            v00 = load_value<float>(P.beta, i00 + k);
-            v01 = load_value<float>(P.beta, i01 + k);
-            v10 = load_value<float>(P.beta, i10 + k);
-            v11 = load_value<float>(P.beta, i11 + k);
+        for (int c = 0; c < 4; c += L) {
+            const int corner = c + (L == 1 ? 0 : s);
+            const uint32_t off = (texel[corner] * static_cast<uint32_t>(D) + k) * esz;
+            const float v = P.beta_f16 ? widen(load_at<_Float16>(P.beta, off)) : load_at<float>(P.beta, off);
+            acc = fmaf(wgt[corner], v, acc);
         }
-        beta[k] = static_cast<float>((w00 * v00 + w01 * v01) + (w10 * v10 + w11 * v11));
+        return grp_sum<L>(acc);
+    };
+    if constexpr (DC > 0) {
+#pragma unroll
+        for (int k = 0; k < DC; ++k)
+            beta_lds[k * kBlockThreads] = component(k);
+    } else {
+        for (int k = 0; k < D; ++k)
+            beta_lds[k * kBlockThreads] = component(k);
     }
 }
 
 __device__ __forceinline__ float sigmoid(float x)
 {
-    return __builtin_amdgcn_rcpf(1.0f + expf(-x));
+    return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-x * kLog2e));
 }
 
-// Colour of one occupied sample: the three uvw records summed over planes
-// (Eq. 4), inner product with beta per channel (Eq. 2), sigmoid.
+// Colour of one occupied sample: beta^T (k^xy + k^yz + k^zx) per channel
+// (Eq. 4 and Eq. 2, summed plane by plane), then a sigmoid.
 template <typename UT, int DC>
 __device__ __forceinline__ void sample_colour(const RenderParams& P, uint32_t t0, uint32_t t1,
-                                              uint32_t t2, const float* beta, float col[3])
+                                              uint32_t t2, const float* beta_lds, float col[3])
 {
+    // beta component k of this lane's ray lives at beta_lds[k * kBlockThreads]
+    auto beta = [&](int k) { return beta_lds[k * kBlockThreads]; };
     if constexpr (DC > 0 && (3 * DC * sizeof(UT)) % 16 == 0) {
         constexpr int NV = 3 * DC;
-        constexpr int NB = NV * static_cast<int>(sizeof(UT));
+        constexpr uint32_t NB = NV * static_cast<uint32_t>(sizeof(UT));
         constexpr int NQ = NB / 16;
-        const uint4* p0 = reinterpret_cast<const uint4*>(static_cast<const char*>(P.uvw[0]) + static_cast<size_t>(t0) * NB);
-        const uint4* p1 = reinterpret_cast<const uint4*>(static_cast<const char*>(P.uvw[1]) + static_cast<size_t>(t1) * NB);
-        const uint4* p2 = reinterpret_cast<const uint4*>(static_cast<const char*>(P.uvw[2]) + static_cast<size_t>(t2) * NB);
-        uint4 q0[NQ], q1[NQ], q2[NQ];
+        const uint32_t texel[3] = {t0, t1, t2};
+        float x[3] = {0.0f, 0.0f, 0.0f};
+        // one plane's record at a time keeps a single record in registers
 #pragma unroll
-        for (int k = 0; k < NQ; ++k) {
-            q0[k] = p0[k];
-            q1[k] = p1[k];
-            q2[k] = p2[k];
+        for (int j = 0; j < 3; ++j) {
+            uint4 q[NQ];
+#pragma unroll
+            for (int k = 0; k < NQ; ++k)
+                q[k] = load_at<uint4>(P.uvw[j], texel[j] * NB + 16u * k);
+            UT rec[NV];
+            __builtin_memcpy(rec, q, NB);
+#pragma unroll
+            for (int c = 0; c < 3; ++c)
+#pragma unroll
+                for (int k = 0; k < DC; ++k)
+                    x[c] = fmaf(beta(k), widen(rec[c * DC + k]), x[c]);
         }
-        UT v0[NV], v1[NV], v2[NV];
-        __builtin_memcpy(v0, q0, NB);
-        __builtin_memcpy(v1, q1, NB);
-        __builtin_memcpy(v2, q2, NB);
 #pragma unroll
-        for (int c = 0; c < 3; ++c) {
-            float x = 0.0f;
-#pragma unroll
-            for (int k = 0; k < DC; ++k) {
-                const float U = (widen(v0[c * DC + k]) + widen(v1[c * DC + k])) + widen(v2[c * DC + k]);
-                x = fmaf(beta[k], U, x);
-            }
-            col[c] = sigmoid(x);
-        }
+        for (int c = 0; c < 3; ++c)
+            col[c] = sigmoid(x[c]);
     } else {
         const int32_t D = P.D;
         const uint32_t nv = 3u * static_cast<uint32_t>(D);
+        const uint32_t esz = static_cast<uint32_t>(sizeof(UT));
         for (int c = 0; c < 3; ++c) {
             float x = 0.0f;
             for (int32_t k = 0; k < D; ++k) {
                 const uint32_t off = static_cast<uint32_t>(c * D + k);
-                const float U = (load_value<UT>(P.uvw[0], t0 * nv + off)
-                                 + load_value<UT>(P.uvw[1], t1 * nv + off))
-                                + load_value<UT>(P.uvw[2], t2 * nv + off);
-                x = fmaf(beta[k], U, x);
+                const float bk = beta(k);
+                x = fmaf(bk, widen(load_at<UT>(P.uvw[0], (t0 * nv + off) * esz)), x);
+                x = fmaf(bk, widen(load_at<UT>(P.uvw[1], (t1 * nv + off) * esz)), x);
+                x = fmaf(bk, widen(load_at<UT>(P.uvw[2], (t2 * nv + off) * esz)), x);
             }
             col[c] = sigmoid(x);
         }
     }
+}
+
+// exp(-tau 2^-32) for a 2^-32 fixed-point optical depth.
+__device__ __forceinline__ float transmittance(uint64_t tau)
+{
+    const float hi = static_cast<float>(static_cast<uint32_t>(tau >> 32));
+    const float lo = static_cast<float>(static_cast<uint32_t>(tau));
+    const float x = fmaf(lo, 0x1p-32f, hi);
+    return __builtin_amdgcn_exp2f(-x * kLog2e);
 }
 
 __device__ __forceinline__ uint32_t fnv1a_word(uint32_t h, uint32_t x)
@@ -247,19 +398,42 @@ __device__ __forceinline__ uint32_t fnv1a_word(uint32_t h, uint32_t x)
     return h;
 }
 
-// Map the hardware workgroup id to a tile so that each XCD (workgroups are
-// dealt round-robin over the 8 XCDs) receives one contiguous run of tiles
-// and its L2 sees spatially coherent gathers.
+#ifndef SQN_XCD_BLOCK
+#define SQN_XCD_BLOCK 4
+#endif
+
+// Map the hardware workgroup id to a tile.  Workgroups are dealt
+// round-robin over the 8 XCDs.  SQN_XCD_BLOCK = 0: each XCD receives one
+// contiguous run of tiles; K > 0: runs of K consecutive tiles are dealt to
+// the XCDs in turn (K = 1 is the hardware order).
 __device__ __forceinline__ int32_t xcd_tile_order(int32_t bid, int32_t n)
 {
     const int32_t xcd = bid & 7, local = bid >> 3;
-    const int32_t per = n >> 3, rem = n & 7;
-    return xcd * per + min(xcd, rem) + local;
+    if constexpr (SQN_XCD_BLOCK == 0) {
+        const int32_t per = n >> 3, rem = n & 7;
+        return xcd * per + min(xcd, rem) + local;
+    } else {
+        constexpr int32_t K = SQN_XCD_BLOCK;
+        const int32_t n_full = (n / (8 * K)) * (8 * K);
+        if (bid >= n_full)
+            return bid;
+        return (xcd + 8 * (local / K)) * K + (local % K);
+    }
 }
 
-template <typename ST, typename UT, int DC, bool STATS>
-__global__ __launch_bounds__(kBlockThreads) void render_kernel(const RenderParams P)
+// Waves per SIMD the register allocation is asked to allow: a single
+// 800x800 view is 10^4 waves at one lane per ray, so occupancy decides how
+// much of the frame runs in a second round.  Larger records need more
+// registers; the targets are the highest that compile without spilling.
+constexpr int waves_per_simd(int record_bytes)
 {
+    return record_bytes == 0 ? 6 : (record_bytes <= 48 ? 8 : (record_bytes <= 96 ? 6 : 5));
+}
+
+template <typename ST, typename UT, int DC, bool STATS, int L>
+__global__ __launch_bounds__(kBlockThreads, waves_per_simd(3 * DC * static_cast<int>(sizeof(UT)))) void render_kernel(const RenderParams P)
+{
+    constexpr int WW = kWaveW(L), WH = kWaveH(L);
     const int32_t g = xcd_tile_order(static_cast<int32_t>(blockIdx.x), P.n_groups);
     const int32_t tiles_per_view = P.tiles_x * P.tiles_y;
     const int32_t view = g / tiles_per_view;
@@ -267,8 +441,11 @@ __global__ __launch_bounds__(kBlockThreads) void render_kernel(const RenderParam
     const int32_t ty = tr / P.tiles_x;
     const int32_t tx = tr - ty * P.tiles_x;
     const int32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int32_t u = tx * kTileW + (wave & 1) * 8 + (lane & 7);
-    const int32_t v = ty * kTileH + (wave >> 1) * 8 + (lane >> 3);
+    const int32_t s = (L == 1) ? 0 : (lane & (L - 1));
+    const int32_t slot = lane / L;
+    const int32_t u = tx * (2 * WW) + (wave & 1) * WW + (slot % WW);
+    const int32_t v = ty * (2 * WH) + (wave >> 1) * WH + (slot / WW);
+    // all L lanes of a ray agree on this, so a group is never split
     if (view >= P.n_views || u >= P.width || v >= P.height)
         return;
 
@@ -299,71 +476,126 @@ __global__ __launch_bounds__(kBlockThreads) void render_kernel(const RenderParam
     int32_t i0, i1;
     clip_to_box(P, o, d, i0, i1);
 
-    float beta[DC > 0 ? DC : 32];
-    lookup_beta<DC>(P, d, beta);
+    // beta of every lane's ray, component-major so that a wave-wide read of
+    // one component touches consecutive LDS words; each lane reads only what
+    // it wrote, so no barrier is needed
+    __shared__ float beta_smem[(DC > 0 ? DC : 32) * kBlockThreads];
+    float* const beta = beta_smem + threadIdx.x;
+    lookup_beta<DC, L>(P, d, s, beta);
 
-    // --- march ---
-    int64_t tau = 0;                 // optical depth before sample i, 2^-32 units
-    double acc_r = 0.0, acc_g = 0.0, acc_b = 0.0, acc_t = 0.0;
-    uint32_t n_inbox = 0, n_occ = 0, hash = 2166136261u;
     const int32_t n_p = P.n_p;
+    const float hi_node = static_cast<float>(n_p - 1);
+    const uint32_t ssz = static_cast<uint32_t>(sizeof(ST));
+    uint64_t tau = 0;              // optical depth before the chunk, 2^-32 units
+    double acc_r = 0.0, acc_g = 0.0, acc_b = 0.0, acc_t = 0.0;
+    int32_t last_live = -1;
+    uint32_t n_inbox = 0, n_occ = 0, hash = 2166136261u;
 
-    int32_t i = i0;
-    float t = (i0 <= i1) ? sample_t(P, stratified, ray_key, i0) : 0.0f;
-    for (; i <= i1; ++i) {
-        if (tau > P.tau_eps)
-            break;
-        const float tn = (i + 1 < N) ? sample_t(P, stratified, ray_key, i + 1) : P.far_t;
+    int32_t base = i0;
+    // t of this lane's sample in the current chunk
+    float t = (base <= i1) ? sample_t(P, stratified, ray_key, base + s) : 0.0f;
+    while (base <= i1 && tau <= static_cast<uint64_t>(P.tau_eps)) {
+        const int32_t i = base + s;
+        const bool in_range = i <= i1;
+        // t_{i+1}: the next lane's t, or for the group's last lane the first
+        // sample of the next chunk (which becomes this lane's next t)
+        const float t_next_chunk = sample_t(P, stratified, ray_key, base + L + s);
+        const float t_first_next = grp_first<L>(t_next_chunk);
+        const float t_lane_next = grp_next<L>(t);
+        float tn = (s == L - 1) ? t_first_next : t_lane_next;
+        if (i + 1 >= N)
+            tn = P.far_t;
+
         float p[3];
-        bool inside = true;
 #pragma unroll
         for (int r = 0; r < 3; ++r) {
             const float td = t * d[r];
             p[r] = o[r] + td;
-            inside = inside && (p[r] >= P.bmin[r]) && (p[r] <= P.bmax[r]);
         }
+        const bool inside = in_range & (p[0] >= P.bmin[0]) & (p[0] <= P.bmax[0]) & (p[1] >= P.bmin[1])
+                            & (p[1] <= P.bmax[1]) & (p[2] >= P.bmin[2]) & (p[2] <= P.bmax[2]);
+        float sigma = 0.0f;
+        uint32_t ix = 0, iy = 0, iz = 0;
         if (inside) {
-            const int32_t ix = nearest_node(p[0], P.bmin[0], P.scale[0], n_p);
-            const int32_t iy = nearest_node(p[1], P.bmin[1], P.scale[1], n_p);
-            const int32_t iz = nearest_node(p[2], P.bmin[2], P.scale[2], n_p);
-            const uint32_t txy = static_cast<uint32_t>(ix * n_p + iy);
-            const uint32_t tyz = static_cast<uint32_t>(iy * n_p + iz);
-            const uint32_t tzx = static_cast<uint32_t>(iz * n_p + ix);
-            const float sxy = load_value<ST>(P.sigma[0], txy);
-            const float syz = load_value<ST>(P.sigma[1], tyz);
-            const float szx = load_value<ST>(P.sigma[2], tzx);
+            ix = nearest_node(p[0], P.bmin[0], P.scale[0], hi_node);
+            iy = nearest_node(p[1], P.bmin[1], P.scale[1], hi_node);
+            iz = nearest_node(p[2], P.bmin[2], P.scale[2], hi_node);
+            const float sxy = widen(load_at<ST>(P.sigma[0], __umul24(ix, n_p) * ssz + iy * ssz));
+            const float syz = widen(load_at<ST>(P.sigma[1], __umul24(iy, n_p) * ssz + iz * ssz));
+            const float szx = widen(load_at<ST>(P.sigma[2], __umul24(iz, n_p) * ssz + ix * ssz));
             float prod = sxy * syz;
             prod = prod * szx;
-            const float sigma = fmaxf(0.0f, prod);
-            if constexpr (STATS)
-                ++n_inbox;
-            if (sigma > 0.0f) {
-                const float gap = fmaxf(0.0f, tn - t);
-                const float delta = gap * dn;
-                const float q = sigma * delta;
-                if constexpr (STATS) {
-                    ++n_occ;
-                    hash = fnv1a_word(hash, static_cast<uint32_t>(i));
-                    hash = fnv1a_word(hash, static_cast<uint32_t>(ix));
-                    hash = fnv1a_word(hash, static_cast<uint32_t>(iy));
-                    hash = fnv1a_word(hash, static_cast<uint32_t>(iz));
+            sigma = fmaxf(0.0f, prod);
+        }
+        float q = 0.0f;
+        uint64_t Q = 0;
+        if (sigma > 0.0f) {
+            const float gap = fmaxf(0.0f, tn - t);
+            const float delta = gap * dn;
+            q = sigma * delta;
+            Q = fixed_q(q);
+        }
+        uint64_t excl, total;
+        grp_scan<L>(Q, s, excl, total);
+        const uint64_t tau_i = tau + excl;
+        // with one lane per ray the loop condition already guarantees
+        // tau_i = tau <= tau_eps and i <= i1
+        const bool live = (L == 1) || (in_range & (tau_i <= static_cast<uint64_t>(P.tau_eps)));
+        const bool occ = live & (sigma > 0.0f);
+        if (occ) {
+            float col[3];
+            sample_colour<UT, DC>(P, __umul24(ix, n_p) + iy, __umul24(iy, n_p) + iz,
+                                  __umul24(iz, n_p) + ix, beta, col);
+            const float T = transmittance(tau_i);
+            const float alpha = -expm1f(-q);
+            const double w = static_cast<double>(T * alpha);
+            acc_r = fma(w, static_cast<double>(col[0]), acc_r);
+            acc_g = fma(w, static_cast<double>(col[1]), acc_g);
+            acc_b = fma(w, static_cast<double>(col[2]), acc_b);
+            acc_t = fma(w, static_cast<double>(t), acc_t);
+        }
+        if (L > 1 && live)
+            last_live = i;
+        if constexpr (STATS) {
+            n_inbox += (live & inside) ? 1u : 0u;
+            n_occ += occ ? 1u : 0u;
+            // FNV-1a over the occupied samples of the group in sample order
+#pragma unroll
+            for (int k = 0; k < L; ++k) {
+                const int src = (lane & ~(L - 1)) + k;
+                const bool o_k = __shfl(occ ? 1 : 0, src) != 0;
+                const uint32_t i_k = static_cast<uint32_t>(__shfl(i, src));
+                const uint32_t x_k = static_cast<uint32_t>(__shfl(static_cast<int>(ix), src));
+                const uint32_t y_k = static_cast<uint32_t>(__shfl(static_cast<int>(iy), src));
+                const uint32_t z_k = static_cast<uint32_t>(__shfl(static_cast<int>(iz), src));
+                if (o_k) {
+                    hash = fnv1a_word(hash, i_k);
+                    hash = fnv1a_word(hash, x_k);
+                    hash = fnv1a_word(hash, y_k);
+                    hash = fnv1a_word(hash, z_k);
                 }
-                float col[3];
-                sample_colour<UT, DC>(P, txy, tyz, tzx, beta, col);
-                const float T = expf(static_cast<float>(tau) * -0x1p-32f);
-                const float alpha = -expm1f(-q);
-                const double w = static_cast<double>(T * alpha);
-                acc_r = fma(w, static_cast<double>(col[0]), acc_r);
-                acc_g = fma(w, static_cast<double>(col[1]), acc_g);
-                acc_b = fma(w, static_cast<double>(col[2]), acc_b);
-                acc_t = fma(w, static_cast<double>(t), acc_t);
-                tau += fixed_q(q);
             }
         }
-        t = tn;
+        tau += total;
+        base += L;
+        t = t_next_chunk;
     }
-    const uint32_t stop = (tau > P.tau_eps) ? static_cast<uint32_t>(i) : static_cast<uint32_t>(N);
 
+    // combine the lanes of the ray
+    acc_r = grp_sum<L>(acc_r);
+    acc_g = grp_sum<L>(acc_g);
+    acc_b = grp_sum<L>(acc_b);
+    acc_t = grp_sum<L>(acc_t);
+    // the first non-live sample: with one lane per ray the loop leaves as
+    // soon as the optical depth crosses, at the index after the last sample
+    const bool terminated = tau > static_cast<uint64_t>(P.tau_eps);
+    const int32_t stop = !terminated ? N : (L == 1 ? base : grp_max<L>(last_live) + 1);
+    if constexpr (STATS) {
+        n_inbox = grp_add<L>(n_inbox);
+        n_occ = grp_add<L>(n_occ);
+    }
+    if (s != 0)
+        return;
     if (P.rgb) {
         P.rgb[3 * ray + 0] = static_cast<float>(acc_r);
         P.rgb[3 * ray + 1] = static_cast<float>(acc_g);
@@ -372,25 +604,38 @@ __global__ __launch_bounds__(kBlockThreads) void render_kernel(const RenderParam
     if (P.depth)
         P.depth[ray] = static_cast<float>(acc_t);
     if constexpr (STATS) {
-        uint4 s;
-        s.x = stop;
-        s.y = n_inbox;
-        s.z = n_occ;
-        s.w = hash;
-        reinterpret_cast<uint4*>(P.stats)[ray] = s;
+        uint4 st;
+        st.x = static_cast<uint32_t>(stop);
+        st.y = n_inbox;
+        st.z = n_occ;
+        st.w = hash;
+        reinterpret_cast<uint4*>(P.stats)[ray] = st;
     }
+}
+
+template <typename ST, typename UT, int DC, int L>
+hipError_t launch_lanes(const RenderParams& p, bool stats, hipStream_t stream)
+{
+    const dim3 grid(static_cast<uint32_t>(p.n_groups));
+    const dim3 block(kBlockThreads);
+    if (stats)
+        render_kernel<ST, UT, DC, true, L><<<grid, block, 0, stream>>>(p);
+    else
+        render_kernel<ST, UT, DC, false, L><<<grid, block, 0, stream>>>(p);
+    return hipGetLastError();
 }
 
 template <typename ST, typename UT, int DC>
 hipError_t launch_typed(const RenderParams& p, bool stats, hipStream_t stream)
 {
-    const dim3 grid(static_cast<uint32_t>(p.n_groups));
-    const dim3 block(kBlockThreads);
-    if (stats)
-        render_kernel<ST, UT, DC, true><<<grid, block, 0, stream>>>(p);
-    else
-        render_kernel<ST, UT, DC, false><<<grid, block, 0, stream>>>(p);
-    return hipGetLastError();
+    switch (p.lanes) {
+    case 1:
+        return launch_lanes<ST, UT, DC, 1>(p, stats, stream);
+    case 2:
+        return launch_lanes<ST, UT, DC, 2>(p, stats, stream);
+    default:
+        return launch_lanes<ST, UT, DC, 4>(p, stats, stream);
+    }
 }
 
 template <typename ST, typename UT>

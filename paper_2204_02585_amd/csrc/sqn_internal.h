@@ -35,7 +35,9 @@ struct RenderParams {
     uint32_t rec_bytes;       // bytes of one uvw record (3D values)
     int64_t tau_eps;          // floor(-ln(eps) 2^32), INT64_MAX for eps = 0
     uint64_t seed;
+    float inv_dt;             // 1 / dt (for the conservative box clip only)
     // launch geometry
+    int32_t lanes;            // lanes per ray: 1, 2 or 4
     int32_t tiles_x, tiles_y; // workgroup tiles per view
     int32_t n_groups;         // workgroups in the grid
 };
@@ -46,9 +48,13 @@ struct RenderParams {
 hipError_t launch_render(const RenderParams& p, int sigma_dtype, int uvw_dtype,
                          bool stats, hipStream_t stream);
 
-// Workgroup geometry used by launch_render (pixels per workgroup tile).
-constexpr int kTileW = 16;
-constexpr int kTileH = 16;
+// Workgroup geometry: 256 threads = 4 wave64; with L lanes per ray a wave
+// holds 64/L rays laid out as a wave tile of kWaveW(L) x kWaveH(L) pixels and
+// a workgroup covers 2 x 2 wave tiles.
 constexpr int kBlockThreads = 256;
+constexpr int kWaveW(int L) { return L == 4 ? 4 : 8; }
+constexpr int kWaveH(int L) { return (64 / L) / kWaveW(L); }
+constexpr int kTileW(int L) { return 2 * kWaveW(L); }
+constexpr int kTileH(int L) { return 2 * kWaveH(L); }
 
 }  // namespace sqn

@@ -11,11 +11,13 @@ def scene_atol(scene):
     return ATOL[scene.config.dtype]
 
 
-def gpu_render(scene, t_eps=None, poses=None, n_samples=None, stats=True):
-    """Render a scene through the C ABI; returns numpy (rgb, depth, stats)."""
+def gpu_render(scene, t_eps=None, poses=None, n_samples=None, stats=True, lanes=0):
+    """Render a scene through the C ABI (lanes per ray: 1, 2, 4 or 0 for the
+    library's choice); returns numpy (rgb, depth, stats)."""
     import torch
     from paper_2204_02585_amd import binding
     caches = binding.caches_from_scene(scene, t_eps=t_eps)
+    caches.set_lanes_per_ray(lanes)
     P = torch.from_numpy(scene.poses if poses is None else poses).cuda()
     N = scene.config.n_samples if n_samples is None else n_samples
     try:
