@@ -45,6 +45,24 @@ def algorithmic_bytes(cfg, n_rays, live_inbox, occupied):
     return n_rays * per_ray + live_inbox * 3 * b + occupied * 3 * 3 * cfg.D * b
 
 
+def measured_traffic(config_name):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE passes (profiles/render_traffic_<workload>.json), scaled by
+    the counters of kernels of known traffic; None when no such file exists
+    or the kernel source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"render_traffic_{config_name}.json")
+    src = os.path.join(ROOT, "paper_2204_02585_amd", "csrc", "render.hip")
+    try:
+        rec = json.load(open(path))
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    except (OSError, ValueError):
+        return None
+    if rec.get("render_hip_sha256_16") != sha:
+        return None
+    return int(rec["traffic_bytes_per_launch"])
+
+
 def cpu_baseline(scene, budget_s=12.0, max_frames=40):
     """The CPU oracle as it stands, on whole frames of the same workload,
     repeated until ~budget_s of wall time (at least one frame)."""
@@ -170,7 +188,8 @@ def main():
         "samples": {"nominal_per_step": nominal, "live_inbox_per_step": live_inbox,
                     "occupied_per_step": occupied},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic(cfg.name) if args.lanes == 0 else None,
                      "algorithmic_bytes_per_launch": int(bytes_alg),
                      "kernel_ms_per_launch": round(ms, 5)},
         "cpu_baseline": base,
