@@ -91,6 +91,8 @@ def main():
     ap.add_argument("--config", default="paper", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--lanes", type=int, default=0,
                     help="lanes of a wavefront per ray (1, 2, 4); 0 = the library's choice")
+    ap.add_argument("--dense", action="store_true",
+                    help="march every sample (no leaps over empty space)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -113,6 +115,7 @@ def main():
     torch.cuda.set_device(dev)
     caches = binding.caches_from_scene(scene, device=dev)
     caches.set_lanes_per_ray(args.lanes)
+    caches.set_empty_space_skipping(not args.dense)
     poses = torch.from_numpy(scene.poses).to(dev)
     B = poses.shape[0]
     rgb = torch.empty((B, cfg.height, cfg.width, 3), dtype=torch.float32, device=dev)
@@ -183,7 +186,8 @@ def main():
                    "views_per_step": B, "width": cfg.width, "height": cfg.height,
                    "samples_per_ray": N, "n_p": cfg.n_p, "D": cfg.D, "cache_dtype": cfg.dtype,
                    "direction_cache": [cfg.n_theta, cfg.n_phi], "t_eps": cfg.t_eps,
-                   "lanes_per_ray": args.lanes or "auto"},
+                   "lanes_per_ray": args.lanes or "auto",
+                   "empty_space_leaps": not args.dense},
         "frames_per_s": round(fps, 2),
         "samples": {"nominal_per_step": nominal, "live_inbox_per_step": live_inbox,
                     "occupied_per_step": occupied},

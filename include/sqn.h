@@ -154,13 +154,23 @@ sqn_status sqn_render_stats(const sqn_caches* caches,
                             void* stream);
 
 /* Launch shape of later renders with this handle: how many lanes of a
- * wavefront share one ray (1, 2 or 4; each lane takes every L-th sample of a
- * chunk of L consecutive samples), or 0 (the default) to choose from the
- * number of rays of each call.  Sample, index and termination decisions are
- * identical for every choice; colour and depth agree up to the rounding of
- * their sums.  Not thread-safe against concurrent renders with the handle.
+ * wavefront share one ray (1 or 4; the L lanes take the L consecutive
+ * samples of a chunk), or 0 (the default) to choose per call from the number
+ * of rays.  Sample, index and termination decisions are identical for every
+ * choice; colour and depth agree up to the rounding of their sums.  Not
+ * thread-safe against concurrent renders with the handle.
  * Errors: SQN_ERR_INVALID_ARG. */
 sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes);
+
+/* Leaps over empty space (1, the default) or a dense march (0).  sigma is
+ * the product of the three planar sigma^j (Sec. 3.2 Eq. 4), so it vanishes
+ * wherever one plane does; sqn_create_caches stores, next to each sigma^j,
+ * the Chebyshev distance to the nearest texel with sigma^j != 0 (capped at
+ * 255), and the march skips every sample whose texel in some plane stays
+ * within that empty square.  Only samples with sigma = 0 are skipped, so
+ * results, sample counts and termination are those of the dense march.
+ * Errors: SQN_ERR_INVALID_ARG. */
+sqn_status sqn_set_empty_space_skipping(sqn_caches* caches, int32_t enable);
 
 /* Bytes of device memory the handle owns. */
 size_t sqn_cache_device_bytes(const sqn_caches* caches);

@@ -19,7 +19,8 @@ SQN_OK, SQN_ERR_INVALID_ARG, SQN_ERR_OUT_OF_MEMORY, SQN_ERR_DEVICE, SQN_ERR_UNSU
 SQN_F32, SQN_F16 = 0, 1
 
 EXPORTS = ("sqn_create_caches", "sqn_render", "sqn_render_stats", "sqn_set_lanes_per_ray",
-           "sqn_cache_device_bytes", "sqn_destroy", "sqn_status_string", "sqn_last_error")
+           "sqn_set_empty_space_skipping", "sqn_cache_device_bytes", "sqn_destroy",
+           "sqn_status_string", "sqn_last_error")
 
 
 class CacheDesc(ctypes.Structure):
@@ -61,6 +62,8 @@ def _load() -> ctypes.CDLL:
                                      vp, vp, vp, vp]
     lib.sqn_set_lanes_per_ray.restype = ctypes.c_int
     lib.sqn_set_lanes_per_ray.argtypes = [vp, i32]
+    lib.sqn_set_empty_space_skipping.restype = ctypes.c_int
+    lib.sqn_set_empty_space_skipping.argtypes = [vp, i32]
     lib.sqn_cache_device_bytes.restype = ctypes.c_size_t
     lib.sqn_cache_device_bytes.argtypes = [vp]
     lib.sqn_destroy.restype = None
@@ -152,8 +155,12 @@ class Caches:
         return int(lib.sqn_cache_device_bytes(self.handle))
 
     def set_lanes_per_ray(self, lanes: int) -> None:
-        """1, 2 or 4 lanes of a wavefront per ray, or 0 to choose per call."""
+        """1 or 4 lanes of a wavefront per ray, or 0 to choose per call."""
         _check(lib.sqn_set_lanes_per_ray(self.handle, int(lanes)))
+
+    def set_empty_space_skipping(self, enable: bool) -> None:
+        """Leaps over empty space (default) or a dense march."""
+        _check(lib.sqn_set_empty_space_skipping(self.handle, 1 if enable else 0))
 
     def close(self) -> None:
         if self._h:

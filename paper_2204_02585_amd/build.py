@@ -9,7 +9,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB_PATH = os.path.join(PKG, "libsqn.so")
-SOURCES = [os.path.join(CSRC, "api.hip"), os.path.join(CSRC, "render.hip")]
+SOURCES = [os.path.join(CSRC, "api.hip"), os.path.join(CSRC, "render.hip"),
+           os.path.join(CSRC, "prepare.hip")]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -23,6 +23,7 @@ struct sqn_caches {
     float scale[3];          // (n_p - 1) / (bmax - bmin), binary32
     int64_t tau_eps;         // floor(-ln(eps) 2^32)
     int32_t lanes;           // lanes per ray, 0 = chosen per call
+    int32_t skip;            // empty-space leaps (one lane per ray)
 };
 
 namespace {
@@ -105,6 +106,7 @@ sqn_status validate_desc(const sqn_cache_desc* d)
     // every plane is addressed with 32-bit byte offsets
     const uint64_t texels = static_cast<uint64_t>(d->n_p) * d->n_p;
     const uint64_t uvw_plane = texels * 3u * d->D * dtype_size(d->uvw_dtype);
+    static_assert(sqn::kDistCap < 65536, "distance must fit the packed record");
     if (uvw_plane >= (uint64_t{1} << 32))
         return fail(SQN_ERR_UNSUPPORTED, "a uvw plane of %llu bytes exceeds 2^32 bytes",
                     static_cast<unsigned long long>(uvw_plane));
@@ -165,10 +167,10 @@ sqn_status validate_render(const sqn_caches* h, const float* poses, int32_t n_po
 }
 
 // Lanes per ray for a call of `rays` rays.  One lane per ray does the least
-// work per sample, but a wave lives as long as its longest ray and 256 CUs x
-// 4 SIMDs x 8 waves hold only 8192 waves: below about 2^20 rays (one 800x800
-// view is 10^4 waves) the last waves run nearly alone, and four lanes per ray
-// (4x the waves, each 4x shorter) finish sooner despite the cross-lane scan.
+// work per sample, but a wave lives as long as its longest ray: below about
+// 2^20 rays (one 800x800 view is 10^4 waves against 8192 resident wave
+// slots) the heaviest waves, not throughput, set the time, and four lanes per
+// ray cut their chains of dependent samples four-fold.
 int choose_lanes(int64_t rays)
 {
     return rays < (int64_t{1} << 20) ? 4 : 1;
@@ -225,7 +227,10 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
     p.tau_eps = h->tau_eps;
     p.seed = h->desc.seed;
     p.inv_dt = 1.0f / p.dt;
-    p.lanes = h->lanes != 0 ? h->lanes : choose_lanes(static_cast<int64_t>(n_poses) * in->width * in->height);
+    const int64_t rays = static_cast<int64_t>(n_poses) * in->width * in->height;
+    p.skip = h->skip;
+    p.lanes = h->lanes != 0 ? h->lanes : choose_lanes(rays);
+    p.leap_margin = 1e-3f;
     const int tw = sqn::kTileW(p.lanes), th = sqn::kTileH(p.lanes);
     p.tiles_x = (in->width + tw - 1) / tw;
     p.tiles_y = (in->height + th - 1) / th;
@@ -260,6 +265,8 @@ sqn_status sqn_create_caches(const sqn_cache_desc* desc, const void* const sigma
 
     const size_t texels = static_cast<size_t>(desc->n_p) * desc->n_p;
     const size_t sigma_bytes = texels * dtype_size(desc->sigma_dtype);
+    // packed (sigma, distance) records: 4 bytes for binary16 sigma, 8 for binary32
+    const size_t packed_bytes = texels * (desc->sigma_dtype == SQN_F16 ? 4 : 8);
     const size_t uvw_bytes = texels * 3 * desc->D * dtype_size(desc->uvw_dtype);
     const size_t beta_bytes = static_cast<size_t>(desc->n_theta) * desc->n_phi * desc->D
                               * dtype_size(desc->beta_dtype);
@@ -278,7 +285,7 @@ sqn_status sqn_create_caches(const sqn_cache_desc* desc, const void* const sigma
     size_t off_sigma[3], off_uvw[3], off_beta, total = 0;
     for (int j = 0; j < 3; ++j) {
         off_sigma[j] = total;
-        total += align(sigma_bytes);
+        total += align(packed_bytes);
     }
     for (int j = 0; j < 3; ++j) {
         off_uvw[j] = total;
@@ -308,10 +315,20 @@ sqn_status sqn_create_caches(const sqn_cache_desc* desc, const void* const sigma
     h->bytes = total;
     char* base = static_cast<char*>(h->block);
     hipStream_t st = static_cast<hipStream_t>(stream);
+    // scratch for the distance transform, freed before returning
+    uint16_t* work = nullptr;
+    e = hipMalloc(reinterpret_cast<void**>(&work), 2 * texels * sizeof(uint16_t));
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        (void)hipFree(h->block);
+        free(h);
+        return fail(SQN_ERR_OUT_OF_MEMORY, "hipMalloc of %zu scratch bytes failed", 2 * texels * sizeof(uint16_t));
+    }
     for (int j = 0; j < 3 && e == hipSuccess; ++j) {
         h->sigma[j] = base + off_sigma[j];
         h->uvw[j] = base + off_uvw[j];
-        e = hipMemcpyAsync(base + off_sigma[j], sigma_planes[j], sigma_bytes, hipMemcpyDeviceToDevice, st);
+        e = sqn::prepare_sigma_plane(sigma_planes[j], desc->sigma_dtype, desc->n_p, base + off_sigma[j],
+                                     work, work + texels, st);
         if (e == hipSuccess)
             e = hipMemcpyAsync(base + off_uvw[j], uvw_planes[j], uvw_bytes, hipMemcpyDeviceToDevice, st);
     }
@@ -320,6 +337,7 @@ sqn_status sqn_create_caches(const sqn_cache_desc* desc, const void* const sigma
         e = hipMemcpyAsync(base + off_beta, beta, beta_bytes, hipMemcpyDeviceToDevice, st);
     if (e == hipSuccess)
         e = hipStreamSynchronize(st);
+    (void)hipFree(work);
     if (e != hipSuccess) {
         (void)hipGetLastError();
         (void)hipFree(h->block);
@@ -329,6 +347,7 @@ sqn_status sqn_create_caches(const sqn_cache_desc* desc, const void* const sigma
     for (int r = 0; r < 3; ++r)
         h->scale[r] = static_cast<float>(desc->n_p - 1) / (desc->bbox_max[r] - desc->bbox_min[r]);
     h->tau_eps = tau_threshold(desc->t_eps);
+    h->skip = 1;
     *out = h;
     g_last_error.clear();
     return SQN_OK;
@@ -353,12 +372,22 @@ sqn_status sqn_render_stats(const sqn_caches* caches, const float* poses, int32_
                          rgb_out, depth_out, ray_stats, stream);
 }
 
+sqn_status sqn_set_empty_space_skipping(sqn_caches* caches, int32_t enable)
+{
+    if (!caches)
+        return fail(SQN_ERR_INVALID_ARG, "caches is NULL");
+    if (enable != 0 && enable != 1)
+        return fail(SQN_ERR_INVALID_ARG, "enable must be 0 or 1 (got %d)", enable);
+    caches->skip = enable;
+    return SQN_OK;
+}
+
 sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes)
 {
     if (!caches)
         return fail(SQN_ERR_INVALID_ARG, "caches is NULL");
-    if (lanes != 0 && lanes != 1 && lanes != 2 && lanes != 4)
-        return fail(SQN_ERR_INVALID_ARG, "lanes per ray must be 0, 1, 2 or 4 (got %d)", lanes);
+    if (lanes != 0 && lanes != 1 && lanes != 4)
+        return fail(SQN_ERR_INVALID_ARG, "lanes per ray must be 0, 1 or 4 (got %d)", lanes);
     caches->lanes = lanes;
     return SQN_OK;
 }

@@ -92,6 +92,18 @@ __device__ __forceinline__ float grp_first(float x)
         return x;
 }
 
+// value of the group's last lane
+template <int L>
+__device__ __forceinline__ int32_t grp_last(int32_t x)
+{
+    if constexpr (L == 2)
+        return static_cast<int32_t>(dpp32<qperm(1, 1, 3, 3)>(static_cast<uint32_t>(x)));
+    else if constexpr (L == 4)
+        return static_cast<int32_t>(dpp32<qperm(3, 3, 3, 3)>(static_cast<uint32_t>(x)));
+    else
+        return x;
+}
+
 // Exclusive prefix sum of q over the group (lane order) and the group total.
 template <int L>
 __device__ __forceinline__ void grp_scan(uint64_t q, int s, uint64_t& excl, uint64_t& total)
@@ -402,6 +414,65 @@ __device__ __forceinline__ uint32_t fnv1a_word(uint32_t h, uint32_t x)
 #define SQN_XCD_BLOCK 4
 #endif
 
+// Packed position record of plane j at a texel: sigma^j and the Chebyshev
+// distance (texels) to the nearest texel with sigma^j != 0 (0 = this one),
+// see prepare.hip.  binary16 sigma: one word (sigma | dist << 16); binary32
+// sigma: two words.
+template <typename ST>
+struct SigmaRecord;
+
+template <>
+struct SigmaRecord<_Float16> {
+    static constexpr uint32_t bytes = 4;
+    static __device__ __forceinline__ void load(const void* plane, uint32_t texel, float& sigma, uint32_t& dist)
+    {
+        const uint32_t w = load_at<uint32_t>(plane, texel * bytes);
+        sigma = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w & 0xffffu)));
+        dist = w >> 16;
+    }
+};
+
+template <>
+struct SigmaRecord<float> {
+    static constexpr uint32_t bytes = 8;
+    static __device__ __forceinline__ void load(const void* plane, uint32_t texel, float& sigma, uint32_t& dist)
+    {
+        const uint2 w = load_at<uint2>(plane, texel * bytes);
+        sigma = __uint_as_float(w.x);
+        dist = w.y;
+    }
+};
+
+// First sample index a leap may land on after sample i, whose nearest nodes
+// are (c[0], c[1], c[2]) and whose plane `j` texel lies at Chebyshev
+// distance D > 0 from every texel with sigma^j != 0.  Every sample whose
+// plane-j texel stays within distance D - 1 is empty; along each of the
+// plane's two axes the grid coordinate g = (p - bmin) scale moves affinely in
+// t (g = g0 + t ds), and the node index stays inside the square while g is
+// below c + D - 1/2 (or above c - D + 1/2 moving down).  The bound is pulled
+// in by `margin` texels (the binary32 position and rounding error of g) and
+// the result by one sample, so every skipped sample is inside the square.
+__device__ __forceinline__ int32_t leap_target(const RenderParams& P, int j, uint32_t D, const uint32_t c[3],
+                                               const float g0[3], const float inv_ds[3], const float ds[3],
+                                               float margin, int32_t i)
+{
+    const float h = static_cast<float>(D) - 0.5f - margin;
+    float t_exit = INFINITY;
+#pragma unroll
+    for (int r = 0; r < 3; ++r) {
+        // plane 0 (xy) uses axes 0, 1; plane 1 (yz) 1, 2; plane 2 (zx) 2, 0
+        const bool used = (r == j) || (r == (j + 1) % 3);
+        const float cr = static_cast<float>(c[r]);
+        const float bound = ds[r] > 0.0f ? cr + h : cr - h;
+        const float tr = (bound - g0[r]) * inv_ds[r];
+        if (used && ds[r] != 0.0f)
+            t_exit = fminf(t_exit, tr);
+    }
+    const float f = floorf((t_exit - P.near_t) * P.inv_dt) - 1.0f;
+    const float lo = static_cast<float>(i + 1), hi = static_cast<float>(P.n_samples);
+    return static_cast<int32_t>(fminf(fmaxf(f, lo), hi));
+}
+
 // Map the hardware workgroup id to a tile.  Workgroups are dealt
 // round-robin over the 8 XCDs.  SQN_XCD_BLOCK = 0: each XCD receives one
 // contiguous run of tiles; K > 0: runs of K consecutive tiles are dealt to
@@ -427,28 +498,19 @@ __device__ __forceinline__ int32_t xcd_tile_order(int32_t bid, int32_t n)
 // registers; the targets are the highest that compile without spilling.
 constexpr int waves_per_simd(int record_bytes)
 {
-    return record_bytes == 0 ? 6 : (record_bytes <= 48 ? 8 : (record_bytes <= 96 ? 6 : 5));
+    return record_bytes == 0 ? 6 : (record_bytes <= 48 ? 8 : (record_bytes <= 96 ? 5 : 4));
 }
 
-template <typename ST, typename UT, int DC, bool STATS, int L>
-__global__ __launch_bounds__(kBlockThreads, waves_per_simd(3 * DC * static_cast<int>(sizeof(UT)))) void render_kernel(const RenderParams P)
+// One ray (or, with L lanes per ray, one L-lane group) at pixel (u, v) of
+// view `view`; `lane` is the lane index in the wave.
+// SKIP: leap over runs of samples that one plane's distance field proves
+// empty (with L lanes per ray, the run that starts at the chunk's last
+// sample decides where the next chunk starts).
+template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP>
+__device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, int32_t u,
+                                           int32_t v, int32_t lane, float* const beta)
 {
-    constexpr int WW = kWaveW(L), WH = kWaveH(L);
-    const int32_t g = xcd_tile_order(static_cast<int32_t>(blockIdx.x), P.n_groups);
-    const int32_t tiles_per_view = P.tiles_x * P.tiles_y;
-    const int32_t view = g / tiles_per_view;
-    const int32_t tr = g - view * tiles_per_view;
-    const int32_t ty = tr / P.tiles_x;
-    const int32_t tx = tr - ty * P.tiles_x;
-    const int32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int32_t s = (L == 1) ? 0 : (lane & (L - 1));
-    const int32_t slot = lane / L;
-    const int32_t u = tx * (2 * WW) + (wave & 1) * WW + (slot % WW);
-    const int32_t v = ty * (2 * WH) + (wave >> 1) * WH + (slot / WW);
-    // all L lanes of a ray agree on this, so a group is never split
-    if (view >= P.n_views || u >= P.width || v >= P.height)
-        return;
-
     const int64_t ray = (static_cast<int64_t>(view) * P.height + v) * P.width + u;
     const int32_t N = P.n_samples;
     const bool stratified = P.stratified != 0;
@@ -476,16 +538,30 @@ __global__ __launch_bounds__(kBlockThreads, waves_per_simd(3 * DC * static_cast<
     int32_t i0, i1;
     clip_to_box(P, o, d, i0, i1);
 
-    // beta of every lane's ray, component-major so that a wave-wide read of
-    // one component touches consecutive LDS words; each lane reads only what
-    // it wrote, so no barrier is needed
-    __shared__ float beta_smem[(DC > 0 ? DC : 32) * kBlockThreads];
-    float* const beta = beta_smem + threadIdx.x;
     lookup_beta<DC, L>(P, d, s, beta);
 
     const int32_t n_p = P.n_p;
     const float hi_node = static_cast<float>(n_p - 1);
-    const uint32_t ssz = static_cast<uint32_t>(sizeof(ST));
+    // grid coordinate of each axis as an affine function of t, for leaps
+    float g0[3], ds[3], inv_ds[3];
+    float leap_margin = 0.0f;
+    if constexpr (SKIP) {
+#pragma unroll
+        for (int r = 0; r < 3; ++r) {
+            g0[r] = (o[r] - P.bmin[r]) * P.scale[r];
+            ds[r] = d[r] * P.scale[r];
+            inv_ds[r] = __builtin_amdgcn_rcpf(ds[r]);
+        }
+        // binary32 rounding of g along the exact path, of g + 1/2 at the node
+        // boundary and of this affine estimate all stay below 2^-20 times
+        // the magnitudes involved (about 16 units in the last place)
+        float mag = static_cast<float>(n_p);
+#pragma unroll
+        for (int r = 0; r < 3; ++r)
+            mag = fmaxf(mag, fabsf(g0[r]) + fabsf(ds[r]) * fabsf(P.far_t)
+                                 + P.scale[r] * (fabsf(P.bmin[r]) + fabsf(P.bmax[r])));
+        leap_margin = P.leap_margin + 0x1p-20f * mag;
+    }
     uint64_t tau = 0;              // optical depth before the chunk, 2^-32 units
     double acc_r = 0.0, acc_g = 0.0, acc_b = 0.0, acc_t = 0.0;
     int32_t last_live = -1;
@@ -516,16 +592,54 @@ __global__ __launch_bounds__(kBlockThreads, waves_per_simd(3 * DC * static_cast<
                             & (p[1] <= P.bmax[1]) & (p[2] >= P.bmin[2]) & (p[2] <= P.bmax[2]);
         float sigma = 0.0f;
         uint32_t ix = 0, iy = 0, iz = 0;
+        int32_t leap = 0;
         if (inside) {
             ix = nearest_node(p[0], P.bmin[0], P.scale[0], hi_node);
             iy = nearest_node(p[1], P.bmin[1], P.scale[1], hi_node);
             iz = nearest_node(p[2], P.bmin[2], P.scale[2], hi_node);
-            const float sxy = widen(load_at<ST>(P.sigma[0], __umul24(ix, n_p) * ssz + iy * ssz));
-            const float syz = widen(load_at<ST>(P.sigma[1], __umul24(iy, n_p) * ssz + iz * ssz));
-            const float szx = widen(load_at<ST>(P.sigma[2], __umul24(iz, n_p) * ssz + ix * ssz));
+            float sxy, syz, szx;
+            uint32_t dxy, dyz, dzx;
+            SigmaRecord<ST>::load(P.sigma[0], __umul24(ix, n_p) + iy, sxy, dxy);
+            SigmaRecord<ST>::load(P.sigma[1], __umul24(iy, n_p) + iz, syz, dyz);
+            SigmaRecord<ST>::load(P.sigma[2], __umul24(iz, n_p) + ix, szx, dzx);
             float prod = sxy * syz;
             prod = prod * szx;
             sigma = fmaxf(0.0f, prod);
+            if constexpr (SKIP) {
+                const uint32_t dmax = max(dxy, max(dyz, dzx));
+                if (dmax != 0) {
+                    const int j = (dxy == dmax) ? 0 : ((dyz == dmax) ? 1 : 2);
+                    const uint32_t c[3] = {ix, iy, iz};
+                    leap = leap_target(P, j, dmax, c, g0, inv_ds, ds, leap_margin, i);
+                }
+            }
+        }
+        // in-box samples among first .. last-1 (diagnostics of a leap)
+        auto count_inbox = [&](int32_t first, int32_t last) {
+            uint32_t n = 0;
+            for (int32_t k = first; k < last; ++k) {
+                const float tk = sample_t(P, stratified, ray_key, k);
+                bool in_k = true;
+#pragma unroll
+                for (int r = 0; r < 3; ++r) {
+                    const float pk = o[r] + tk * d[r];
+                    in_k = in_k & (pk >= P.bmin[r]) & (pk <= P.bmax[r]);
+                }
+                n += in_k ? 1u : 0u;
+            }
+            return n;
+        };
+        if constexpr (SKIP && L == 1) {
+            if (leap != 0) {
+                // samples i .. leap-1 are empty: sample i has sigma^j = 0 in
+                // the plane with distance dmax, the rest stay within its
+                // empty square
+                if constexpr (STATS)
+                    n_inbox += count_inbox(i, leap);
+                base = leap;
+                t = sample_t(P, stratified, ray_key, base);
+                continue;
+            }
         }
         float q = 0.0f;
         uint64_t Q = 0;
@@ -577,8 +691,21 @@ __global__ __launch_bounds__(kBlockThreads, waves_per_simd(3 * DC * static_cast<
             }
         }
         tau += total;
-        base += L;
-        t = t_next_chunk;
+        int32_t next = base + L;
+        if constexpr (SKIP && L > 1) {
+            // every lane's empty run [i, leap) is a valid leap: the next chunk
+            // starts at the furthest one that ends past this chunk
+            const int32_t last_leap = grp_max<L>(leap);
+            if (last_leap > next && tau <= static_cast<uint64_t>(P.tau_eps)) {
+                if constexpr (STATS) {
+                    if (s == 0)
+                        n_inbox += count_inbox(next, last_leap);
+                }
+                next = last_leap;
+            }
+        }
+        t = (next == base + L) ? t_next_chunk : sample_t(P, stratified, ray_key, next + s);
+        base = next;
     }
 
     // combine the lanes of the ray
@@ -613,29 +740,51 @@ __global__ __launch_bounds__(kBlockThreads, waves_per_simd(3 * DC * static_cast<
     }
 }
 
-template <typename ST, typename UT, int DC, int L>
-hipError_t launch_lanes(const RenderParams& p, bool stats, hipStream_t stream)
+// Launch shapes: L = 1 or 4 lanes per ray over workgroup tiles of
+// kTileW(L) x kTileH(L) pixels, with or without leaps over empty space.
+template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP>
+__global__ __launch_bounds__(kBlockThreads, waves_per_simd(3 * DC * static_cast<int>(sizeof(UT)))) void render_kernel(const RenderParams P)
+{
+    // beta of every lane's ray, component-major so that a wave-wide read of
+    // one component touches consecutive LDS words; each lane reads only what
+    // it wrote, so no barrier is needed
+    __shared__ float beta_smem[(DC > 0 ? DC : 32) * kBlockThreads];
+    const int32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int32_t tile = xcd_tile_order(static_cast<int32_t>(blockIdx.x), P.n_groups);
+    const int32_t tiles_per_view = P.tiles_x * P.tiles_y;
+    const int32_t view = tile / tiles_per_view;
+    const int32_t tr = tile - view * tiles_per_view;
+    const int32_t ty = tr / P.tiles_x;
+    const int32_t tx = tr - ty * P.tiles_x;
+    constexpr int32_t WW = kWaveW(L), WH = kWaveH(L);
+    const int32_t slot = lane / L;
+    const int32_t u = tx * kTileW(L) + (wave & 1) * WW + (slot % WW);
+    const int32_t v = ty * kTileH(L) + (wave >> 1) * WH + (slot / WW);
+    // all lanes of a ray agree on this, so a lane group is never split
+    if (view < P.n_views && u < P.width && v < P.height)
+        render_ray<ST, UT, DC, STATS, L, SKIP>(P, view, u, v, lane, beta_smem + threadIdx.x);
+}
+
+template <typename ST, typename UT, int DC, int L, bool SKIP>
+hipError_t launch_shape(const RenderParams& p, bool stats, hipStream_t stream)
 {
     const dim3 grid(static_cast<uint32_t>(p.n_groups));
     const dim3 block(kBlockThreads);
     if (stats)
-        render_kernel<ST, UT, DC, true, L><<<grid, block, 0, stream>>>(p);
+        render_kernel<ST, UT, DC, true, L, SKIP><<<grid, block, 0, stream>>>(p);
     else
-        render_kernel<ST, UT, DC, false, L><<<grid, block, 0, stream>>>(p);
+        render_kernel<ST, UT, DC, false, L, SKIP><<<grid, block, 0, stream>>>(p);
     return hipGetLastError();
 }
 
 template <typename ST, typename UT, int DC>
 hipError_t launch_typed(const RenderParams& p, bool stats, hipStream_t stream)
 {
-    switch (p.lanes) {
-    case 1:
-        return launch_lanes<ST, UT, DC, 1>(p, stats, stream);
-    case 2:
-        return launch_lanes<ST, UT, DC, 2>(p, stats, stream);
-    default:
-        return launch_lanes<ST, UT, DC, 4>(p, stats, stream);
-    }
+    if (p.lanes == 1)
+        return p.skip ? launch_shape<ST, UT, DC, 1, true>(p, stats, stream)
+                      : launch_shape<ST, UT, DC, 1, false>(p, stats, stream);
+    return p.skip ? launch_shape<ST, UT, DC, 4, true>(p, stats, stream)
+                  : launch_shape<ST, UT, DC, 4, false>(p, stats, stream);
 }
 
 template <typename ST, typename UT>

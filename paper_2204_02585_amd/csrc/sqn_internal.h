@@ -12,7 +12,7 @@ namespace sqn {
 // Everything one render launch reads, passed by value as the kernel argument.
 struct RenderParams {
     // caches (library-owned device memory)
-    const void* sigma[3];     // [n_p][n_p], planes xy, yz, zx
+    const void* sigma[3];     // [n_p][n_p] packed (sigma, distance) records, planes xy, yz, zx
     const void* uvw[3];       // [n_p][n_p][3D] records
     const void* beta;         // [n_theta][n_phi][D]
     // camera batch and outputs (caller-owned device memory)
@@ -38,6 +38,8 @@ struct RenderParams {
     float inv_dt;             // 1 / dt (for the conservative box clip only)
     // launch geometry
     int32_t lanes;            // lanes per ray: 1, 2 or 4
+    int32_t skip;             // 1: one lane per ray with empty-space leaps
+    float leap_margin;        // texels a leap keeps from its square's edge
     int32_t tiles_x, tiles_y; // workgroup tiles per view
     int32_t n_groups;         // workgroups in the grid
 };
@@ -47,6 +49,15 @@ struct RenderParams {
 // caller.  Returns the launch status.
 hipError_t launch_render(const RenderParams& p, int sigma_dtype, int uvw_dtype,
                          bool stats, hipStream_t stream);
+
+// Cap of the stored Chebyshev distance to the nearest occupied texel.
+constexpr int32_t kDistCap = 255;
+
+// Pack sigma plane j (n_p x n_p of sigma_dtype, device memory) into
+// `packed` (4-byte records for binary16 sigma, 8-byte for binary32) with the
+// capped distance transform; work_f and work_dist are n_p^2 scratch words.
+hipError_t prepare_sigma_plane(const void* sigma, int sigma_dtype, int32_t n_p, void* packed,
+                               uint16_t* work_f, uint16_t* work_dist, hipStream_t stream);
 
 // Workgroup geometry: 256 threads = 4 wave64; with L lanes per ray a wave
 // holds 64/L rays laid out as a wave tile of kWaveW(L) x kWaveH(L) pixels and

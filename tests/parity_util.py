@@ -11,13 +11,20 @@ def scene_atol(scene):
     return ATOL[scene.config.dtype]
 
 
-def gpu_render(scene, t_eps=None, poses=None, n_samples=None, stats=True, lanes=0):
-    """Render a scene through the C ABI (lanes per ray: 1, 2, 4 or 0 for the
-    library's choice); returns numpy (rgb, depth, stats)."""
+# launch variants: library default (leaps, lanes chosen per call), leaps with
+# 1 or 4 lanes per ray, and the dense march with 1 or 4 lanes per ray
+MODES = {"auto": (0, True), "skip1": (1, True), "skip4": (4, True), "L1": (1, False), "L4": (4, False)}
+
+
+def gpu_render(scene, t_eps=None, poses=None, n_samples=None, stats=True, mode="auto"):
+    """Render a scene through the C ABI in one of MODES; returns numpy
+    (rgb, depth, stats)."""
     import torch
     from paper_2204_02585_amd import binding
     caches = binding.caches_from_scene(scene, t_eps=t_eps)
+    lanes, skip = MODES[mode]
     caches.set_lanes_per_ray(lanes)
+    caches.set_empty_space_skipping(skip)
     P = torch.from_numpy(scene.poses if poses is None else poses).cuda()
     N = scene.config.n_samples if n_samples is None else n_samples
     try:

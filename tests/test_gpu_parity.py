@@ -27,17 +27,17 @@ def _gpu():
 
 # ---------------------------------------------------------------- small sizes
 
-LANES = [1, 2, 4]
+MODES = list(pu.MODES)
 
 
-@pytest.mark.parametrize("lanes", LANES)
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("t_eps", [1e-4, 0.0])
-def test_tiny_full_frame(t_eps, lanes):
+def test_tiny_full_frame(t_eps, mode):
     sc = scenes.make_scene("tiny")
-    gpu = pu.gpu_render(sc, t_eps=t_eps, lanes=lanes)
+    gpu = pu.gpu_render(sc, t_eps=t_eps, mode=mode)
     ref = oracle.render_scene(sc, t_eps=t_eps)
     ids = np.arange(ref.size)
-    pu.compare(gpu, ref, ids, pu.scene_atol(sc), f"tiny eps={t_eps} L={lanes}")
+    pu.compare(gpu, ref, ids, pu.scene_atol(sc), f"tiny eps={t_eps} {mode}")
     assert (ref["n_occ"] > 0).sum() > 100
 
 
@@ -47,31 +47,31 @@ def _small(name, **kw):
     return scenes.make_scene(cfg)
 
 
-@pytest.mark.parametrize("lanes", LANES)
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("W,H", [(37, 23), (1, 1), (16, 16), (17, 1), (1, 33)])
-def test_ragged_and_degenerate_image_sizes(W, H, lanes):
+def test_ragged_and_degenerate_image_sizes(W, H, mode):
     sc = _small("tiny", width=W, height=H, focal=1.25 * max(W, H))
-    gpu = pu.gpu_render(sc, lanes=lanes)
+    gpu = pu.gpu_render(sc, mode=mode)
     ref = oracle.render_scene(sc)
     pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), f"{W}x{H}")
 
 
-@pytest.mark.parametrize("lanes", LANES)
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("N", [1, 2, 3, 7, 384, 4096])
-def test_sample_counts(N, lanes):
+def test_sample_counts(N, mode):
     sc = _small("tiny", width=24, height=20, n_samples=N)
-    gpu = pu.gpu_render(sc, lanes=lanes)
+    gpu = pu.gpu_render(sc, mode=mode)
     ref = oracle.render_scene(sc)
     pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), f"N={N}")
 
 
-@pytest.mark.parametrize("lanes", LANES)
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("D", [1, 3, 8, 16, 32])
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
-def test_component_counts_and_dtypes(D, dtype, lanes):
+def test_component_counts_and_dtypes(D, dtype, mode):
     """Specialised (D = 8, 16) and generic kernels, both storage types."""
     sc = _small("tiny", width=40, height=40, D=D, dtype=dtype, n_p=48, n_theta=9, n_phi=12)
-    gpu = pu.gpu_render(sc, lanes=lanes)
+    gpu = pu.gpu_render(sc, mode=mode)
     ref = oracle.render_scene(sc)
     pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), f"D={D} {dtype}")
 
@@ -86,25 +86,25 @@ def test_paper_precision_mix():
     pu.compare(gpu, ref, np.arange(ref.size), 1e-5, "sigma f32 / uvw f16")
 
 
-@pytest.mark.parametrize("lanes", LANES)
-def test_stratified_small(lanes):
+@pytest.mark.parametrize("mode", MODES)
+def test_stratified_small(mode):
     sc = _small("tiny", width=32, height=32, stratified=True)
-    gpu = pu.gpu_render(sc, lanes=lanes)
+    gpu = pu.gpu_render(sc, mode=mode)
     ref = oracle.render_scene(sc)
     pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), "stratified")
 
 
-@pytest.mark.parametrize("lanes", LANES)
-def test_multi_view_batch_small(lanes):
+@pytest.mark.parametrize("mode", MODES)
+def test_multi_view_batch_small(mode):
     sc = _small("tiny", width=20, height=12)
     poses = scenes.spiral_poses(7)
-    gpu = pu.gpu_render(sc, poses=poses, lanes=lanes)
+    gpu = pu.gpu_render(sc, poses=poses, mode=mode)
     ref = oracle.render_scene(sc, poses=poses)
     pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), "7 views")
 
 
-@pytest.mark.parametrize("lanes", LANES)
-def test_camera_inside_box_and_axis_rays(lanes):
+@pytest.mark.parametrize("mode", MODES)
+def test_camera_inside_box_and_axis_rays(mode):
     """Rays that start inside the box, run along box faces or have zero
     direction components (the clip's exact special case)."""
     sc = _small("tiny", width=9, height=9, focal=4.0)
@@ -117,17 +117,17 @@ def test_camera_inside_box_and_axis_rays(lanes):
     P[2, :, 0], P[2, :, 1], P[2, :, 2], P[2, :, 3] = (1, 0, 0), (0, 0, 1), (0, -1, 0), (1.5, -4, -1.5)
     # looking straight down -z from above
     P[3, :, 0], P[3, :, 1], P[3, :, 2], P[3, :, 3] = (1, 0, 0), (0, 1, 0), (0, 0, 1), (0.2, 0.1, 4)
-    gpu = pu.gpu_render(sc, poses=P, lanes=lanes)
+    gpu = pu.gpu_render(sc, poses=P, mode=mode)
     ref = oracle.render_scene(sc, poses=P)
     pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), "inside/axis")
     assert ref["n_inbox"].sum() > 0
 
 
-@pytest.mark.parametrize("lanes", LANES)
-def test_dense_scene_terminates(lanes):
+@pytest.mark.parametrize("mode", MODES)
+def test_dense_scene_terminates(mode):
     """sigma_max 2000: most rays stop within a few samples."""
     sc = _small("tiny", width=48, height=48, sigma_max=2000.0)
-    gpu = pu.gpu_render(sc, lanes=lanes)
+    gpu = pu.gpu_render(sc, mode=mode)
     ref = oracle.render_scene(sc)
     pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), "dense")
     assert (ref["stop"] < sc.config.n_samples).mean() > 0.1
@@ -147,14 +147,25 @@ def test_empty_batch_is_noop():
         caches.close()
 
 
+def test_large_ragged_two_views():
+    """Default launch on two 1000 x 700 views (not a multiple of the tile
+    size) at a small sample count."""
+    sc = _small("tiny", width=1000, height=700, n_samples=24, focal=1250.0)
+    poses = scenes.spiral_poses(2)
+    gpu = pu.gpu_render(sc, poses=poses, mode="auto")
+    ref = oracle.render_scene(sc, poses=poses)
+    pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), "2x1000x700")
+    assert (ref["n_occ"] > 0).sum() > 1000
+
+
 # ------------------------------------------------------- full workload sizes
 
-@pytest.mark.parametrize("lanes", [0] + LANES)
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("name,n_random", [("paper", 40000), ("large", 40000)])
-def test_full_size_single_view(name, n_random, lanes):
+def test_full_size_single_view(name, n_random, mode):
     sc = scenes.make_scene(name)
     cfg = sc.config
-    gpu = pu.gpu_render(sc, lanes=lanes)
+    gpu = pu.gpu_render(sc, mode=mode)
     ids = pu.sample_ray_ids(1, cfg.height, cfg.width, n_random, seed=cfg.number)
     ref = oracle.render_scene(sc, ray_ids=ids)
     pu.compare(gpu, ref, ids, pu.scene_atol(sc), name)
@@ -174,11 +185,11 @@ def test_full_size_batch():
     pu.compare(gpu, ref, ids, pu.scene_atol(sc), "batch")
 
 
-@pytest.mark.parametrize("lanes", [0, 1, 4])
-def test_full_size_stress(lanes):
+@pytest.mark.parametrize("mode", ["auto", "skip1", "skip4", "L1"])
+def test_full_size_stress(mode):
     sc = scenes.make_scene("stress")
     cfg = sc.config
-    gpu = pu.gpu_render(sc, lanes=lanes)
+    gpu = pu.gpu_render(sc, mode=mode)
     ids = pu.sample_ray_ids(1, cfg.height, cfg.width, 20000, seed=5)
     ref = oracle.render_scene(sc, ray_ids=ids)
     pu.compare(gpu, ref, ids, pu.scene_atol(sc), "stress")
@@ -280,19 +291,24 @@ def test_create_rejects_bad_descriptions_and_undersized_arrays():
         short.free()
 
 
-def test_lanes_option_validation():
+def test_launch_option_validation():
     from paper_2204_02585_amd import binding
     sc = scenes.make_scene("tiny")
     caches = binding.caches_from_scene(sc)
     try:
-        for bad in (3, -1, 8):
+        for bad in (2, 3, -1, 8):
             with pytest.raises(binding.SqnError):
                 caches.set_lanes_per_ray(bad)
-        for good in (0, 1, 2, 4):
+        for good in (0, 1, 4):
             caches.set_lanes_per_ray(good)
+        for bad in (2, -1):
+            assert binding.lib.sqn_set_empty_space_skipping(caches.handle, bad) == binding.SQN_ERR_INVALID_ARG
+        caches.set_empty_space_skipping(False)
+        caches.set_empty_space_skipping(True)
     finally:
         caches.close()
     assert binding.lib.sqn_set_lanes_per_ray(None, 1) == binding.SQN_ERR_INVALID_ARG
+    assert binding.lib.sqn_set_empty_space_skipping(None, 1) == binding.SQN_ERR_INVALID_ARG
 
 
 def test_create_out_of_memory_hook(monkeypatch):
