@@ -7,8 +7,8 @@ path without fused multiply-add, binary64 value path); this module only
 compiles it and marshals numpy arrays.
 
 Functions and the passages they follow:
-  render        -- Eq. 1 compositing of Eq. 4 / Eq. 2 cached fields along
-                   pinhole rays (Sec. 3.1, 3.2, 3.3, 3.4)
+  render        -- Eq. 1 compositing of Eq. 4 (or Eq. 5) / Eq. 2 cached
+                   fields along pinhole rays (Sec. 3.1, 3.2, 3.3, 3.4)
   tau_eps_q     -- transmittance threshold T >= eps as a fixed-point optical
                    depth bound
   half_to_double, splitmix64 -- input decoding and the stratified-sampling
@@ -54,7 +54,10 @@ class _Scene(ctypes.Structure):
                 ("t_eps", ctypes.c_float), ("pad0", ctypes.c_int32),
                 ("seed", ctypes.c_uint64),
                 ("sigma", ctypes.c_void_p * 3), ("uvw", ctypes.c_void_p * 3),
-                ("beta", ctypes.c_void_p)]
+                ("beta", ctypes.c_void_p),
+                ("d_sigma", ctypes.c_int32), ("b_sigma", ctypes.c_float),
+                ("w_sigma", ctypes.c_void_p), ("w_uvw", ctypes.c_void_p),
+                ("b_uvw", ctypes.c_void_p)]
 
 
 class _Camera(ctypes.Structure):
@@ -106,10 +109,12 @@ def splitmix64(seed: int, counter: int) -> int:
 
 
 def cache_nbytes(n_p: int, D: int, n_theta: int, n_phi: int,
-                 sigma_bytes: int, uvw_bytes: int, beta_bytes: int) -> int:
-    """Sec. 3.3: three n_p x n_p planes of sigma^j (1 value) and u^j, v^j,
-    w^j (D values each), plus n_theta x n_phi x D direction weights."""
-    return 3 * n_p * n_p * (sigma_bytes + 3 * D * uvw_bytes) + n_theta * n_phi * D * beta_bytes
+                 sigma_bytes: int, uvw_bytes: int, beta_bytes: int, d_sigma: int = 1) -> int:
+    """Sec. 3.3: three n_p x n_p planes of sigma^j (1 value; D_sigma values
+    for the Eq. 5 decoder) and u^j, v^j, w^j (D values each), plus
+    n_theta x n_phi x D direction weights."""
+    return (3 * n_p * n_p * (d_sigma * sigma_bytes + 3 * D * uvw_bytes)
+            + n_theta * n_phi * D * beta_bytes)
 
 
 def _dtype_flag(a: np.ndarray) -> int:
@@ -124,10 +129,14 @@ def render(sigma: Sequence[np.ndarray], uvw: Sequence[np.ndarray], beta: np.ndar
            poses: np.ndarray, intrinsics: dict, near: float, far: float, n_samples: int,
            bbox_min, bbox_max, t_eps: float = 1e-4, stratified: bool = False,
            seed: int = 0, ray_ids: Optional[np.ndarray] = None,
-           n_threads: Optional[int] = None) -> np.ndarray:
+           n_threads: Optional[int] = None, decoder=None) -> np.ndarray:
     """Render rays on the CPU; returns a structured array of RAY_DTYPE
     (rgb, depth, acc, tau_end, stop, n_inbox, n_occ, hash), one per ray,
-    in ray-id order ((b*H + v)*W + u) or in the order of `ray_ids`."""
+    in ray-id order ((b*H + v)*W + u) or in the order of `ray_ids`.
+
+    decoder: None for Eq. 4, or an object with w_sigma [3 D_sigma],
+    b_sigma, w_uvw [3][D][3D] and b_uvw [3][D] for Eq. 5; then each
+    sigma[j] is [n_p][n_p][D_sigma]."""
     lib = _load()
     sigma = [np.ascontiguousarray(a) for a in sigma]
     uvw = [np.ascontiguousarray(a) for a in uvw]
@@ -135,8 +144,10 @@ def render(sigma: Sequence[np.ndarray], uvw: Sequence[np.ndarray], beta: np.ndar
     poses = np.ascontiguousarray(poses, dtype=np.float32).reshape(-1, 3, 4)
     n_p = sigma[0].shape[0]
     D = uvw[0].shape[-1] // 3
+    d_sigma = 0 if decoder is None else sigma[0].shape[2]
+    want = (n_p, n_p) if decoder is None else (n_p, n_p, d_sigma)
     for a in sigma:
-        assert a.shape == (n_p, n_p) and a.dtype == sigma[0].dtype
+        assert a.shape == want and a.dtype == sigma[0].dtype
     for a in uvw:
         assert a.shape == (n_p, n_p, 3 * D) and a.dtype == uvw[0].dtype
     assert beta.ndim == 3 and beta.shape[2] == D
@@ -155,6 +166,17 @@ def render(sigma: Sequence[np.ndarray], uvw: Sequence[np.ndarray], beta: np.ndar
         sc.sigma[j] = sigma[j].ctypes.data
         sc.uvw[j] = uvw[j].ctypes.data
     sc.beta = beta.ctypes.data
+    if decoder is not None:
+        w_sigma = np.ascontiguousarray(decoder.w_sigma, dtype=np.float32)
+        w_uvw = np.ascontiguousarray(decoder.w_uvw, dtype=np.float32)
+        b_uvw = np.ascontiguousarray(decoder.b_uvw, dtype=np.float32)
+        assert d_sigma >= 1 and w_sigma.shape == (3 * d_sigma,)
+        assert w_uvw.shape == (3, D, 3 * D) and b_uvw.shape == (3, D)
+        sc.d_sigma = d_sigma
+        sc.b_sigma = float(decoder.b_sigma)
+        sc.w_sigma = w_sigma.ctypes.data
+        sc.w_uvw = w_uvw.ctypes.data
+        sc.b_uvw = b_uvw.ctypes.data
 
     cam = _Camera(float(intrinsics["fx"]), float(intrinsics["fy"]), float(intrinsics["cx"]),
                   float(intrinsics["cy"]), int(intrinsics["width"]), int(intrinsics["height"]))
@@ -187,4 +209,5 @@ def render_scene(scene, ray_ids=None, n_threads=None, n_samples=None, t_eps=None
                   scene.bbox_min, scene.bbox_max,
                   t_eps=cfg.t_eps if t_eps is None else t_eps,
                   stratified=cfg.stratified if stratified is None else stratified,
-                  seed=scene.seed, ray_ids=ray_ids, n_threads=n_threads)
+                  seed=scene.seed, ray_ids=ray_ids, n_threads=n_threads,
+                  decoder=getattr(scene, "decoder", None))

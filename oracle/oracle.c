@@ -84,6 +84,57 @@ static uint32_t fnv1a_word(uint32_t h, uint32_t x)
     return h;
 }
 
+/* ---- Eq. 5, the alternative ("alt") decoder ----------------------------- */
+
+/* Density: sigma = W_sigma concat(sigma^xy, sigma^yz, sigma^zx) + b_sigma,
+ * then max(0, .) so that Eq. 1 sees a non-negative density.  The binary32
+ * evaluation order is fixed here because sigma decides the optical depth and
+ * hence termination (the paper gives none): for each plane the partial dot
+ * product of its D_sigma channels with its block of W_sigma, as a chain of
+ * correctly rounded fused multiply-adds starting from zero in channel order;
+ * then the three partial sums added in plane order; then the bias.  A NaN
+ * sum counts as zero density. */
+static float alt_sigma(const oracle_scene* sc, const size_t texel[3])
+{
+    const int32_t ds = sc->d_sigma;
+    float part[3];
+    for (int j = 0; j < 3; ++j) {
+        float s = 0.0f;
+        for (int32_t c = 0; c < ds; ++c) {
+            float f = cache_value(sc->sigma[j], sc->sigma_f16, texel[j] * (size_t)ds + c);
+            s = fmaf(sc->w_sigma[j * ds + c], f, s);
+        }
+        part[j] = s;
+    }
+    float pre = part[0] + part[1];
+    pre = pre + part[2];
+    pre = pre + sc->b_sigma;
+    return pre > 0.0f ? pre : 0.0f;
+}
+
+/* Colour logits (binary64): for each channel k in (u, v, w) the decoded
+ * vector k = W_k concat(k^xy, k^yz, k^zx) + b_k (Eq. 5), then its inner
+ * product with beta (Eq. 2). */
+static void alt_logits(const oracle_scene* sc, const size_t rec[3], const double* beta,
+                       double x[3])
+{
+    const int32_t D = sc->D;
+    for (int c = 0; c < 3; ++c) {
+        const float* W = sc->w_uvw + (size_t)c * D * 3 * D;
+        double sum = 0.0;
+        for (int32_t d = 0; d < D; ++d) {
+            double k = (double)sc->b_uvw[c * D + d];
+            for (int j = 0; j < 3; ++j)
+                for (int32_t e = 0; e < D; ++e) {
+                    double f = cache_value64(sc->uvw[j], sc->uvw_f16, rec[j] + (size_t)c * D + e);
+                    k += (double)W[(size_t)d * 3 * D + (size_t)j * D + e] * f;
+                }
+            sum += beta[d] * k;
+        }
+        x[c] = sum;
+    }
+}
+
 /* ---- one ray ------------------------------------------------------------ */
 
 typedef struct {
@@ -216,19 +267,27 @@ static void render_ray(const job_t* J, int64_t ray_id, oracle_ray* out)
 
         float sigma = 0.0f;
         int32_t ix = 0, iy = 0, iz = 0;
+        size_t texel[3] = {0, 0, 0};
         if (inside) {
             n_inbox++;
             ix = nearest_node(p[0], sc->bmin[0], J->scale[0], n_p);
             iy = nearest_node(p[1], sc->bmin[1], J->scale[1], n_p);
             iz = nearest_node(p[2], sc->bmin[2], J->scale[2], n_p);
-            /* Eq. 4: sigma is the product of the three planar densities,
-             * plane (x,y) at [ix][iy], (y,z) at [iy][iz], (z,x) at [iz][ix]. */
-            float sxy = cache_value(sc->sigma[0], sc->sigma_f16, (size_t)ix * n_p + iy);
-            float syz = cache_value(sc->sigma[1], sc->sigma_f16, (size_t)iy * n_p + iz);
-            float szx = cache_value(sc->sigma[2], sc->sigma_f16, (size_t)iz * n_p + ix);
-            float prod = sxy * syz;
-            prod = prod * szx;
-            sigma = fmaxf(0.0f, prod);
+            /* Plane (x,y) at [ix][iy], (y,z) at [iy][iz], (z,x) at [iz][ix]. */
+            texel[0] = (size_t)ix * n_p + iy;
+            texel[1] = (size_t)iy * n_p + iz;
+            texel[2] = (size_t)iz * n_p + ix;
+            if (sc->d_sigma > 0) {
+                sigma = alt_sigma(sc, texel);
+            } else {
+                /* Eq. 4: sigma is the product of the three planar densities. */
+                float sxy = cache_value(sc->sigma[0], sc->sigma_f16, texel[0]);
+                float syz = cache_value(sc->sigma[1], sc->sigma_f16, texel[1]);
+                float szx = cache_value(sc->sigma[2], sc->sigma_f16, texel[2]);
+                float prod = sxy * syz;
+                prod = prod * szx;
+                sigma = fmaxf(0.0f, prod);
+            }
         }
 
         /* delta_i: distance to the next sample (the far plane after the
@@ -247,24 +306,27 @@ static void render_ray(const job_t* J, int64_t ray_id, oracle_ray* out)
             hash = fnv1a_word(hash, (uint32_t)iy);
             hash = fnv1a_word(hash, (uint32_t)iz);
 
-            /* Eq. 4 (sum of the planar k^j) and Eq. 2 (inner product with
-             * beta), then a sigmoid per channel. */
+            /* Eq. 4 (sum of the planar k^j) or Eq. 5, and Eq. 2 (inner
+             * product with beta), then a sigmoid per channel. */
             size_t rec[3];
-            rec[0] = ((size_t)ix * n_p + iy) * (size_t)(3 * D);
-            rec[1] = ((size_t)iy * n_p + iz) * (size_t)(3 * D);
-            rec[2] = ((size_t)iz * n_p + ix) * (size_t)(3 * D);
-            double col[3];
-            for (int c = 0; c < 3; ++c) {
-                double x = 0.0;
-                for (int32_t k = 0; k < D; ++k) {
-                    size_t off = (size_t)c * D + k;
-                    double kxy = cache_value64(sc->uvw[0], sc->uvw_f16, rec[0] + off);
-                    double kyz = cache_value64(sc->uvw[1], sc->uvw_f16, rec[1] + off);
-                    double kzx = cache_value64(sc->uvw[2], sc->uvw_f16, rec[2] + off);
-                    x += beta[k] * ((kxy + kyz) + kzx);
-                }
-                col[c] = 1.0 / (1.0 + exp(-x));
+            for (int j = 0; j < 3; ++j)
+                rec[j] = texel[j] * (size_t)(3 * D);
+            double x[3] = {0.0, 0.0, 0.0};
+            if (sc->d_sigma > 0) {
+                alt_logits(sc, rec, beta, x);
+            } else {
+                for (int c = 0; c < 3; ++c)
+                    for (int32_t k = 0; k < D; ++k) {
+                        size_t off = (size_t)c * D + k;
+                        double kxy = cache_value64(sc->uvw[0], sc->uvw_f16, rec[0] + off);
+                        double kyz = cache_value64(sc->uvw[1], sc->uvw_f16, rec[1] + off);
+                        double kzx = cache_value64(sc->uvw[2], sc->uvw_f16, rec[2] + off);
+                        x[c] += beta[k] * ((kxy + kyz) + kzx);
+                    }
             }
+            double col[3];
+            for (int c = 0; c < 3; ++c)
+                col[c] = 1.0 / (1.0 + exp(-x[c]));
 
             /* Eq. 1: w_i = T_i (1 - exp(-sigma_i delta_i)). */
             double T = exp(-(double)tau * 0x1p-32);
@@ -327,6 +389,8 @@ int oracle_render(const oracle_scene* sc, const float* poses, int32_t n_poses,
     if (!sc || !poses || !cam || !out || n_poses < 1 || n_samples < 1)
         return -1;
     if (sc->n_p < 2 || sc->D < 1 || sc->D > 64 || sc->n_theta < 2 || sc->n_phi < 2)
+        return -1;
+    if (sc->d_sigma < 0 || (sc->d_sigma > 0 && (!sc->w_sigma || !sc->w_uvw || !sc->b_uvw)))
         return -1;
     if (cam->width < 1 || cam->height < 1 || !(near_t < far_t))
         return -1;

@@ -8,13 +8,16 @@
  *
  * What it computes, per pixel ray (SqueezeNeRF Sec. 3.1 Eq. 1-2, Sec. 3.2
  * Eq. 4, Sec. 3.3, Sec. 3.4):
- *   - a pinhole ray through the pixel centre (Sec. 3.1, "a ray is projected
- *     from the camera center that passes through that pixel");
+ *   - a pinhole ray from the camera centre through the pixel centre
+ *     (Sec. 3.1);
  *   - N samples between the near and far planes (Sec. 3.1), uniform or
  *     stratified with a seeded SplitMix64 offset per bin;
  *   - nearest-neighbour lookup of sigma^j and (u^j, v^j, w^j) in the three
  *     position sub-caches (Sec. 3.4), fused by Eq. 4: sigma = product of the
- *     sigma^j, k = sum of the k^j;
+ *     sigma^j, k = sum of the k^j; or, for the alternative decoder
+ *     ("SqueezeNeRF (alt)", Sec. 3.2 Eq. 5), sigma^j a D_sigma-vector and
+ *     sigma = max(0, W_sigma concat(sigma^j) + b_sigma),
+ *     k = W_k concat(k^j) + b_k for each k in (u, v, w);
  *   - bilinear lookup of beta in the direction cache at (theta, phi)
  *     (Sec. 3.4);
  *   - colour c = sigmoid(beta^T (u, v, w)) (Eq. 2 followed by a sigmoid);
@@ -24,8 +27,10 @@
  *
  * Precision: every step that decides an integer (ray, sample position, grid
  * index, termination) is evaluated in IEEE binary32 with one rounding per
- * operation and no fused multiply-add; colour, transmittance, weights and
- * the sums are evaluated in binary64.
+ * operation and no fused multiply-add, except the Eq. 5 density, which is
+ * defined as chains of correctly rounded binary32 fused multiply-adds (see
+ * oracle.c); colour, transmittance, weights and the sums are evaluated in
+ * binary64.
  */
 #ifndef SQN_ORACLE_H
 #define SQN_ORACLE_H
@@ -50,8 +55,15 @@ typedef struct {
     int32_t pad0;
     uint64_t seed;          /* stratified-sampling seed                       */
     const void* sigma[3];   /* [n_p][n_p] each, planes xy, yz, zx             */
+                            /* ([n_p][n_p][d_sigma] when d_sigma > 0)         */
     const void* uvw[3];     /* [n_p][n_p][3D] each: u[0..D) v[0..D) w[0..D)   */
     const void* beta;       /* [n_theta][n_phi][D]                            */
+    /* Eq. 5 decoder (used when d_sigma > 0), binary32: */
+    int32_t d_sigma;        /* 0: Eq. 4; > 0: channels of each sigma^j        */
+    float b_sigma;          /* density bias                                   */
+    const float* w_sigma;   /* [3 d_sigma], columns in concat order xy,yz,zx  */
+    const float* w_uvw;     /* [3][D][3D]: W_u, W_v, W_w, row-major           */
+    const float* b_uvw;     /* [3][D]: b_u, b_v, b_w                          */
 } oracle_scene;
 
 typedef struct {

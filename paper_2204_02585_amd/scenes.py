@@ -9,9 +9,12 @@ Cache layout (SqueezeNeRF Sec. 3.3, "Caching"): for each ordered pair
 j in {(x,y), (y,z), (z,x)} one dense n_p x n_p grid over the scene box holds
 sigma^j (1 value) and u^j, v^j, w^j (D values each), i.e. 3D+1 values per
 texel; the direction cache holds D values (beta) on an n_theta x n_phi grid.
+The alternative decoder ("SqueezeNeRF (alt)", Sec. 3.2 Eq. 5) stores D_sigma
+values of sigma^j per texel instead (3D + D_sigma values) and a linear map.
 
 Array shapes produced here (the logical layout the C ABI accepts):
   sigma[j] : [n_p][n_p]        plane j indexed [first axis][second axis]
+             ([n_p][n_p][D_sigma] for the linear decoder)
   uvw[j]   : [n_p][n_p][3D]    record = u[0..D) v[0..D) w[0..D)
   beta     : [n_theta][n_phi][D]
   poses    : [B][3][4] float32 camera-to-world [R | c], camera looks down -z
@@ -61,6 +64,7 @@ class Config:
     stratified: bool = False
     t_eps: float = 1e-4
     focal: Optional[float] = None  # default 1.25 * width
+    sigma_channels: int = 0        # 0: Eq. 4 product of scalar sigma^j; > 0: Eq. 5 linear map
 
     @property
     def fx(self) -> float:
@@ -86,6 +90,15 @@ CONFIGS = {
     # 1920x1080, N=384 stratified, k=2048, D=16, direction cache 512x512
     "stress": Config("stress", 5, 1920, 1080, 384, 2048, 16, 512, 512, "f16", 256, 50.0,
                      0.02, 0.5, stratified=True),
+    # as "tiny" with the Eq. 5 decoder (D_sigma = 12) and 48 blobs
+    "tiny_alt": Config("tiny_alt", 8, 64, 64, 64, 64, 8, 32, 32, "f32", 48, 50.0, 0.1, 0.4,
+                       focal=80.0, sigma_channels=12),
+    # "SqueezeNeRF (alt)" decoder (Eq. 5, D_sigma = 12) on the paper shape
+    "alt": Config("alt", 6, 800, 800, 192, 256, 8, 128, 128, "f16", 64, 50.0, 0.1, 0.4,
+                  sigma_channels=12),
+    # the alt decoder at the paper's alt cache size (n_p = 512, n_d = 256)
+    "alt512": Config("alt512", 7, 800, 800, 192, 512, 8, 256, 256, "f16", 64, 50.0, 0.1, 0.4,
+                     sigma_channels=12),
 }
 
 
@@ -200,6 +213,70 @@ def np_dtype(name: str):
     return {"f32": np.float32, "f16": np.float16}[name]
 
 
+def bake_linear_sigma_planes(n_p: int, blobs: Blobs, channels: int, dtype=np.float32,
+                             bmin=BOX_MIN, bmax=BOX_MAX, s_frac: float = 0.25,
+                             rho_frac: float = 0.6) -> List[np.ndarray]:
+    """Planar features for the linear decoder: blob b adds its planar
+    Gaussian exp(-(da^2 + db^2) / (4 s^2)) (cut to 0 beyond rho) to channel
+    b mod channels of every plane.  With all-ones weights and a threshold
+    bias (linear_sigma_map) a point is dense only where its three planar
+    projections all lie near blobs."""
+    planes = []
+    for (ra, rb) in PLANE_AXES:
+        xa = node_coords(n_p, bmin[ra], bmax[ra])
+        xb = node_coords(n_p, bmin[rb], bmax[rb])
+        acc = np.zeros((n_p, n_p, channels), dtype=np.float64)
+        step_a = (bmax[ra] - bmin[ra]) / (n_p - 1)
+        step_b = (bmax[rb] - bmin[rb]) / (n_p - 1)
+        for k, (c, r) in enumerate(zip(blobs.centre, blobs.radius)):
+            s = s_frac * r
+            rho = rho_frac * r
+            ca, cb = c[ra], c[rb]
+            a0 = max(0, int(math.floor((ca - rho - bmin[ra]) / step_a)))
+            a1 = min(n_p - 1, int(math.ceil((ca + rho - bmin[ra]) / step_a)))
+            b0 = max(0, int(math.floor((cb - rho - bmin[rb]) / step_b)))
+            b1 = min(n_p - 1, int(math.ceil((cb + rho - bmin[rb]) / step_b)))
+            if a0 > a1 or b0 > b1:
+                continue
+            da = xa[a0:a1 + 1, None] - ca
+            db = xb[None, b0:b1 + 1] - cb
+            r2 = da * da + db * db
+            f = np.exp(-r2 / (4.0 * s * s))
+            f[r2 > rho * rho] = 0.0
+            acc[a0:a1 + 1, b0:b1 + 1, k % channels] += f
+        planes.append(acc.astype(dtype))
+    return planes
+
+
+@dataclasses.dataclass
+class LinearDecoder:
+    """Eq. 5 parameters: sigma = W_sigma concat(sigma^xy, sigma^yz, sigma^zx)
+    + b_sigma and, for each k in (u, v, w), k = W_k concat(k^xy, k^yz, k^zx)
+    + b_k.  Shapes: w_sigma [3 Ds], b_sigma scalar, w_uvw [3][D][3D],
+    b_uvw [3][D] (binary32)."""
+    w_sigma: np.ndarray
+    b_sigma: float
+    w_uvw: np.ndarray
+    b_uvw: np.ndarray
+
+
+def linear_decoder(channels: int, D: int, sigma_max: float, seed: int,
+                   threshold: float = 2.2) -> LinearDecoder:
+    """Density weights scale * U(0.8, 1.2) per channel, with scale such that
+    a point sitting on one blob in all three planes (feature sum 3) gets
+    about sigma_max, and a bias that cuts everything below a feature sum of
+    about `threshold`; radiance maps uniform in +-1/sqrt(3D), biases in
+    +-0.1."""
+    scale = sigma_max / (3.0 - threshold)
+    rng = np.random.Generator(np.random.PCG64(seed))
+    w_sigma = (scale * rng.uniform(0.8, 1.2, size=3 * channels)).astype(np.float32)
+    b_sigma = float(np.float32(-scale * threshold))
+    lim = 1.0 / math.sqrt(3 * D)
+    w_uvw = rng.uniform(-lim, lim, size=(3, D, 3 * D)).astype(np.float32)
+    b_uvw = rng.uniform(-0.1, 0.1, size=(3, D)).astype(np.float32)
+    return LinearDecoder(w_sigma, b_sigma, w_uvw, b_uvw)
+
+
 @dataclasses.dataclass
 class Scene:
     """Everything one render call needs, as host arrays."""
@@ -213,6 +290,7 @@ class Scene:
     bbox_min: tuple = BOX_MIN
     bbox_max: tuple = BOX_MAX
     seed: int = 0
+    decoder: Optional[LinearDecoder] = None   # set for the linear (alt) decoder
 
     @property
     def intrinsics(self):
@@ -221,6 +299,8 @@ class Scene:
                     width=c.width, height=c.height)
 
     def cache_nbytes(self) -> int:
+        """Bytes of the cache arrays (Sec. 3.3: 3 n_p^2 (3D + D_sigma) values
+        plus n_d^2 D; the linear decoder's weights are not counted)."""
         return (sum(a.nbytes for a in self.sigma) + sum(a.nbytes for a in self.uvw)
                 + self.beta.nbytes)
 
@@ -234,10 +314,15 @@ def make_scene(name_or_config, n_poses: Optional[int] = None) -> Scene:
     n = cfg.number
     dt = np_dtype(cfg.dtype)
     blobs = make_blobs(cfg.n_blobs, cfg.sigma_max, cfg.r_min, cfg.r_max, 1000 + n)
-    sigma = bake_sigma_planes(cfg.n_p, blobs, dt)
+    decoder = None
+    if cfg.sigma_channels > 0:
+        sigma = bake_linear_sigma_planes(cfg.n_p, blobs, cfg.sigma_channels, dt)
+        decoder = linear_decoder(cfg.sigma_channels, cfg.D, cfg.sigma_max, 6000 + n)
+    else:
+        sigma = bake_sigma_planes(cfg.n_p, blobs, dt)
     rng_uvw = np.random.Generator(np.random.PCG64(2000 + n))
     uvw = [uniform_pm1((cfg.n_p, cfg.n_p, 3 * cfg.D), dt, rng_uvw) for _ in range(3)]
     rng_beta = np.random.Generator(np.random.PCG64(3000 + n))
     beta = uniform_pm1((cfg.n_theta, cfg.n_phi, cfg.D), dt, rng_beta)
     poses = single_pose() if cfg.n_poses == 1 else spiral_poses(cfg.n_poses)
-    return Scene(cfg, sigma, uvw, beta, poses, seed=4000 + n)
+    return Scene(cfg, sigma, uvw, beta, poses, seed=4000 + n, decoder=decoder)

@@ -90,6 +90,16 @@ def test_cache_size_formula_matches_printed_sizes():
     assert abs(b1k / mib - g["cache_mb_np1024_nd64_D8"]) / g["cache_mb_np1024_nd64_D8"] < 0.01
 
 
+def test_alt_cache_size_formula_matches_printed_size():
+    """Sec. 3.3 / Table 2: SqueezeNeRF (alt) stores 3 n_p^2 (3D + D_sigma)
+    fp16 values plus n_d^2 D fp16 direction values; n_p = 512, n_d = 256,
+    D = 8, D_sigma = 12 gives 57.67e6 bytes, printed as 58MB."""
+    g = _golden_printed()
+    b = oracle.cache_nbytes(512, 8, 256, 256, 2, 2, 2, d_sigma=12)
+    assert b == 3 * 512 * 512 * 36 * 2 + 256 * 256 * 8 * 2 == 57_671_680
+    assert abs(b / 1e6 - g["cache_mb_alt_np512_nd256"]) < 0.5
+
+
 def test_work_unit_matches_printed_sample_count():
     """Sec. 1: 800x800 pixels x 192 samples = 122.88 million queries."""
     from paper_2204_02585_amd import scenes
@@ -241,6 +251,173 @@ def test_inner_product_over_D_components():
 
 
 # --------------------------------------------------------------------------
+# Sec. 3.2 Eq. 5: the alternative decoder, on the axis-ray scene above
+# --------------------------------------------------------------------------
+
+class Decoder:
+    """Eq. 5 parameters: w_sigma [3 D_sigma], b_sigma, w_uvw [3][D][3D],
+    b_uvw [3][D]."""
+
+    def __init__(self, w_sigma, b_sigma, w_uvw, b_uvw):
+        self.w_sigma = np.asarray(w_sigma, dtype=np.float32)
+        self.b_sigma = float(b_sigma)
+        self.w_uvw = np.asarray(w_uvw, dtype=np.float32)
+        self.b_uvw = np.asarray(b_uvw, dtype=np.float32)
+
+
+def identity_blocks(D):
+    """W_k = [I I I]: k = k^xy + k^yz + k^zx, the Eq. 4 sum."""
+    w = np.zeros((3, D, 3 * D), np.float32)
+    for c in range(3):
+        for j in range(3):
+            w[c, :, j * D:(j + 1) * D] = np.eye(D)
+    return w
+
+
+def _render_axis_alt(case, sigma, dec, uvw=None, beta=None, D=1, t_eps=0.0):
+    _, direction, origin, _ = AXIS_CASES[case]
+    if uvw is None:
+        uvw = uvw_const(3, D, [(0, 0, 0)] * 3)
+    if beta is None:
+        beta = beta_const(0.0, D=D)
+    return oracle.render(sigma, uvw, beta, centre_ray_pose(direction, origin), ONE_PIXEL,
+                         1.0, 5.0, 8, (-1, -1, -1), (1, 1, 1), t_eps=t_eps, decoder=dec)[0]
+
+
+def _pattern_planes(case, d_sigma=1, fill=1.0, channel=0):
+    """Planes [3][3][d_sigma] holding `fill`, except channel `channel` of the
+    varied plane of `case`, which holds the axis pattern."""
+    j = AXIS_CASES[case][0]
+    planes = [np.full((3, 3, d_sigma), fill, np.float32) for _ in range(3)]
+    planes[j][:, :, channel] = _pattern()
+    return planes
+
+
+@pytest.mark.parametrize("case", sorted(AXIS_CASES))
+def test_alt_reduces_to_eq4_fusion(case):
+    """Eq. 5 with D_sigma = 1, W_sigma = (1, 1, 1), b_sigma = -2 on planes
+    holding the pattern p in one plane and 1 in the other two gives
+    sigma = (p + 1 + 1) - 2 = p, exactly the Eq. 4 product p * 1 * 1; with
+    W_k = [I I I] and b_k = 0, k = k^xy + k^yz + k^zx as in Eq. 4.  The
+    render must then match the Eq. 4 axis case and the fusion values
+    (0.625, 0.5, -1) of test_fusion_sums_uvw_over_planes."""
+    uvw = uvw_const(3, 1, [(0.5, 1.0, -0.5), (0.25, -1.0, -0.25), (-0.125, 0.5, -0.25)])
+    dec = Decoder([1.0, 1.0, 1.0], -2.0, identity_blocks(1), np.zeros((3, 1)))
+    r = _render_axis_alt(case, _pattern_planes(case), dec, uvw=uvw, beta=beta_const(1.0))
+    acc, depth, tau = _axis_expected()
+    assert r["stop"] == 8 and r["n_inbox"] == 5 and r["n_occ"] == 5
+    assert r["tau_end"] == int(tau * 2 ** 32)
+    assert abs(r["acc"] - acc) < 1e-12 and abs(r["depth"] - depth) < 1e-12
+    want = np.array([sigmoid(0.625), sigmoid(0.5), sigmoid(-1.0)]) * acc
+    assert np.allclose(r["rgb"], want, atol=1e-12, rtol=0)
+    words = []
+    for i, (ix, iy, iz) in zip(range(2, 7), AXIS_CASES[case][3]):
+        words += [i, ix, iy, iz]
+    assert r["hash"] == fnv1a(words)
+
+
+@pytest.mark.parametrize("case,channel", [("xy", 2), ("yz", 0), ("zx", 1)])
+def test_alt_density_reads_the_selected_channel_and_plane(case, channel):
+    """Eq. 5 with D_sigma = 3 and a one-hot W_sigma on column
+    3 j + channel of the concat: sigma = that channel of plane j.  Every
+    other channel of every plane holds 100, which a wrong record offset,
+    plane order or column would pick up."""
+    j = AXIS_CASES[case][0]
+    planes = _pattern_planes(case, d_sigma=3, fill=100.0, channel=channel)
+    w = np.zeros(9, np.float32)
+    w[3 * j + channel] = 1.0
+    r = _render_axis_alt(case, planes, Decoder(w, 0.0, identity_blocks(1), np.zeros((3, 1))))
+    acc, depth, tau = _axis_expected()
+    assert r["n_occ"] == 5 and r["tau_end"] == int(tau * 2 ** 32)
+    assert abs(r["acc"] - acc) < 1e-12 and abs(r["depth"] - depth) < 1e-12
+
+
+def test_alt_density_bias_and_clamp():
+    """sigma = max(0, (p + 1 + 1) + b).  b = -3.5: sigma = p - 1.5 =
+    1/4, 1/2, 1/2, 3/4, 3/4 on the pattern values 7/4, 2, 2, 9/4, 9/4, so
+    q = sigma / 2 and the optical depth ends at 11/8.  b = -5: p - 3 < 0
+    everywhere, so the ray is empty."""
+    dec = Decoder([1.0, 1.0, 1.0], -3.5, identity_blocks(1), np.zeros((3, 1)))
+    r = _render_axis_alt("xy", _pattern_planes("xy"), dec)
+    assert r["n_occ"] == 5 and r["tau_end"] == 11 * 2 ** 29
+    qs = [0.125, 0.25, 0.25, 0.375, 0.375]
+    taus = np.concatenate([[0.0], np.cumsum(qs)[:-1]])
+    acc = sum(math.exp(-t) * (1 - math.exp(-q)) for t, q in zip(taus, qs))
+    assert abs(r["acc"] - acc) < 1e-12
+    dec.b_sigma = -5.0
+    r = _render_axis_alt("xy", _pattern_planes("xy"), dec)
+    assert r["n_occ"] == 0 and r["n_inbox"] == 5 and r["tau_end"] == 0
+    assert r["acc"] == 0 and np.all(r["rgb"] == 0) and r["hash"] == FNV_OFFSET
+
+
+def test_alt_radiance_map_rows_columns_and_blocks():
+    """Eq. 5, k = W_k concat(k^xy, k^yz, k^zx) + b_k, then Eq. 2 with D = 3.
+    Plane j holds, for channel c in (u, v, w) and component e,
+    (j + 1) + (3c + e + 1)/16 on every texel.  beta = (1/2, -1, 2).
+      W_u: one at row 2, column 3 (plane yz, u_0 = 2 + 1/16);
+           b_u = (1/4, 0, 0) -> k_u = (1/4, 0, 33/16),
+           logit = 1/8 + 33/8 = 4.25
+      W_v: one at row 0, column 7 (plane zx, v_1 = 3 + 5/16);
+           b_v = 0 -> logit = 53/32 = 1.65625
+      W_w: zero; b_w = (0, 1/2, 0) -> logit = -1/2
+    A transposed W_k, a swapped block or channel changes these values."""
+    D = 3
+    uvw = []
+    for j in range(3):
+        rec = np.array([(j + 1) + (3 * c + e + 1) / 16.0 for c in range(3) for e in range(D)],
+                       np.float32)
+        uvw.append(np.broadcast_to(rec, (3, 3, 3 * D)).copy())
+    w = np.zeros((3, D, 3 * D), np.float32)
+    w[0, 2, 3] = 1.0
+    w[1, 0, 7] = 1.0
+    b = np.zeros((3, D), np.float32)
+    b[0, 0] = 0.25
+    b[2, 1] = 0.5
+    beta = np.broadcast_to(np.array([0.5, -1.0, 2.0], np.float32), (2, 2, D)).copy()
+    dec = Decoder([1.0, 1.0, 1.0], -2.0, w, b)
+    r = _render_axis_alt("xy", _pattern_planes("xy"), dec, uvw=uvw, beta=beta, D=D)
+    acc, _, _ = _axis_expected()
+    want = np.array([sigmoid(4.25), sigmoid(1.65625), sigmoid(-0.5)]) * acc
+    assert np.allclose(r["rgb"], want, atol=1e-12, rtol=0)
+
+
+# Reading of Eq. 5's binary32 density (the paper fixes no order): per plane a
+# chain of fused multiply-adds over the channels starting from zero, then
+# (part_xy + part_yz) + part_zx, then + b_sigma.  On the y-axis ray every
+# in-box sample has delta = 1/2, so sigma = 2^-24 gives Q = 2^7 per sample.
+
+def _const_alt_planes(values):
+    """values[j] = the channel vector held by every texel of plane j."""
+    return [np.broadcast_to(np.asarray(v, np.float32), (3, 3, len(v))).copy() for v in values]
+
+
+def test_alt_density_uses_fused_multiply_add_chain():
+    """Plane xy channels (1 + 2^-11, 1 + 2^-12) with weights
+    (-1, 1 + 2^-12): fma(1 + 2^-12, 1 + 2^-12, -(1 + 2^-11)) = 2^-24 exactly,
+    while a rounded product first (1 + 2^-11) would cancel to 0."""
+    planes = _const_alt_planes([(1 + 2.0 ** -11, 1 + 2.0 ** -12), (0.0, 0.0), (0.0, 0.0)])
+    dec = Decoder([-1.0, 1 + 2.0 ** -12, 1.0, 1.0, 1.0, 1.0], 0.0, identity_blocks(1),
+                  np.zeros((3, 1)))
+    r = _render_axis_alt("xy", planes, dec)
+    assert r["n_occ"] == 5 and r["tau_end"] == 5 * 2 ** 7
+
+
+@pytest.mark.parametrize("parts,bias,n_occ,q_units", [
+    # (1 + 3*2^-26) rounds to 1, then - 1 = 0: empty
+    ((1.0, 3 * 2.0 ** -26, -1.0), 0.0, 0, 0),
+    # the bias comes last: ((1 + 3*2^-26) + 0) - 1 = 0: empty
+    ((1.0, 3 * 2.0 ** -26, 0.0), -1.0, 0, 0),
+    # (-1 + 1) + 3*2^-26 = 3*2^-26 > 0: q = 3*2^-27, Q = 96
+    ((-1.0, 1.0, 3 * 2.0 ** -26), 0.0, 5, 96),
+])
+def test_alt_density_summation_order(parts, bias, n_occ, q_units):
+    planes = _const_alt_planes([(p,) for p in parts])
+    dec = Decoder([1.0, 1.0, 1.0], bias, identity_blocks(1), np.zeros((3, 1)))
+    r = _render_axis_alt("xy", planes, dec)
+    assert r["n_occ"] == n_occ and r["tau_end"] == 5 * q_units
+
+
+# --------------------------------------------------------------------------
 # Eq. 1: closed forms for uniform density
 # --------------------------------------------------------------------------
 
@@ -375,10 +552,10 @@ def test_image_orientation():
 # invariants on the seeded synthetic scenes
 # --------------------------------------------------------------------------
 
-@pytest.fixture(scope="module")
-def tiny_scene():
+@pytest.fixture(scope="module", params=["tiny", "tiny_alt"])
+def tiny_scene(request):
     from paper_2204_02585_amd import scenes
-    return scenes.make_scene("tiny")
+    return scenes.make_scene(request.param)
 
 
 def test_invariants_on_tiny_scene(tiny_scene):
