@@ -8,7 +8,8 @@
  *   2. places N samples between the near and far planes (Sec. 3.1, 3.4),
  *   3. looks up sigma^j and (u^j, v^j, w^j) in the three factorized position
  *      sub-caches with nearest-neighbour lookup (Sec. 3.3, 3.4) and fuses
- *      them by Eq. 4 (sigma = product, k = sum over the planes),
+ *      them by Eq. 4 (sigma = product, k = sum over the planes) or, for
+ *      caches made by sqn_create_linear_caches, by Eq. 5 (linear maps),
  *   4. looks up beta in the direction cache with bilinear interpolation
  *      (Sec. 3.4),
  *   5. forms colour c = sigmoid(beta^T (u, v, w)) (Eq. 2, then a sigmoid),
@@ -31,7 +32,8 @@
  *     nodes are vertex-aligned over the box (node 0 on bbox_min, node n_p-1
  *     on bbox_max); nearest node = floor(g + 1/2) clamped, g = (p - bmin)
  *     (n_p - 1) / (bmax - bmin); samples outside the box have sigma = 0;
- *   - sigma = max(0, (sigma^xy sigma^yz) sigma^zx);
+ *   - sigma = max(0, (sigma^xy sigma^yz) sigma^zx) (Eq. 4; Eq. 5: see
+ *     sqn_linear_decoder);
  *   - direction cache: theta = polar angle from world +z on n_theta nodes
  *     spanning [0, pi] (clamped), phi = atan2(d_y, d_x) on n_phi periodic
  *     nodes at -pi + b 2 pi / n_phi;
@@ -118,6 +120,42 @@ sqn_status sqn_create_caches(const sqn_cache_desc* desc,
                              void* stream,
                              sqn_caches** out);
 
+/* Parameters of the alternative decoder "SqueezeNeRF (alt)" (Sec. 3.2
+ * Eq. 5), binary32, in host memory:
+ *   sigma = max(0, W_sigma concat(sigma^xy, sigma^yz, sigma^zx) + b_sigma),
+ *   k     = W_k concat(k^xy, k^yz, k^zx) + b_k   for k in (u, v, w),
+ * with each sigma^j a d_sigma-vector (the paper uses 12) and each k^j a
+ * D-vector.  The max(0, .) keeps Eq. 1's density non-negative (the paper
+ * states no activation).  The binary32 density is evaluated as: for each
+ * plane j, s^j = a chain of fused multiply-adds over its channels in order,
+ * starting from zero (s = fma(W_sigma[j d_sigma + c], sigma^j[c], s)); then
+ * ((s^xy + s^yz) + s^zx) + b_sigma, each sum rounded; a NaN counts as 0. */
+typedef struct {
+    int32_t d_sigma;        /* channels of each sigma^j, 1..64                 */
+    float b_sigma;          /* density bias                                    */
+    const float* w_sigma;   /* [3 d_sigma], columns in concat order xy, yz, zx */
+    const float* w_uvw;     /* [3][D][3D]: W_u, W_v, W_w, row-major            */
+    const float* b_uvw;     /* [3][D]: b_u, b_v, b_w                           */
+} sqn_linear_decoder;
+
+/* sqn_create_caches for the Eq. 5 decoder.
+ *   decoder:         host pointer, read during the call only;
+ *   sigma_planes[j]: device pointer, [n_p][n_p][d_sigma] of desc->sigma_dtype
+ *                    (the paper stores every alt cache value in fp16);
+ *   uvw_planes, beta, stream, out: as for sqn_create_caches.
+ * The handle keeps, per plane texel, s^j in binary32 (the channels are
+ * folded with W_sigma here) and the radiance weights; renders use four lanes
+ * per ray.  Weights and biases must be finite.
+ * Errors: as sqn_create_caches, plus SQN_ERR_INVALID_ARG for a NULL or
+ * non-finite decoder parameter or d_sigma outside [1, 64]. */
+sqn_status sqn_create_linear_caches(const sqn_cache_desc* desc,
+                                    const sqn_linear_decoder* decoder,
+                                    const void* const sigma_planes[3],
+                                    const void* const uvw_planes[3],
+                                    const void* beta,
+                                    void* stream,
+                                    sqn_caches** out);
+
 /* Render n_poses views (Sec. 3.4, Eq. 1).
  *   poses:      device pointer, [n_poses][3][4] binary32 camera-to-world;
  *   intrinsics: host pointer, read during the call only;
@@ -159,7 +197,8 @@ sqn_status sqn_render_stats(const sqn_caches* caches,
  * of rays.  Sample, index and termination decisions are identical for every
  * choice; colour and depth agree up to the rounding of their sums.  Not
  * thread-safe against concurrent renders with the handle.
- * Errors: SQN_ERR_INVALID_ARG. */
+ * Errors: SQN_ERR_INVALID_ARG; SQN_ERR_UNSUPPORTED for 1 on a handle made
+ * by sqn_create_linear_caches (always four lanes). */
 sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes);
 
 /* Leaps over empty space (1, the default) or a dense march (0).  sigma is
@@ -167,8 +206,11 @@ sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes);
  * wherever one plane does; sqn_create_caches stores, next to each sigma^j,
  * the Chebyshev distance to the nearest texel with sigma^j != 0 (capped at
  * 255), and the march skips every sample whose texel in some plane stays
- * within that empty square.  Only samples with sigma = 0 are skipped, so
- * results, sample counts and termination are those of the dense march.
+ * within that empty square.  For the Eq. 5 decoder a texel of plane j counts
+ * as empty when its s^j plus the largest s^k the other two planes hold along
+ * the row or column the texel shares with them, plus b_sigma, is <= 0 in the
+ * same binary32 order.  Only samples with sigma = 0 are skipped, so results,
+ * sample counts and termination are those of the dense march.
  * Errors: SQN_ERR_INVALID_ARG. */
 sqn_status sqn_set_empty_space_skipping(sqn_caches* caches, int32_t enable);
 

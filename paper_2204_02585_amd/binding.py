@@ -18,9 +18,9 @@ LIB_PATH = os.path.join(_PKG, "libsqn.so")
 SQN_OK, SQN_ERR_INVALID_ARG, SQN_ERR_OUT_OF_MEMORY, SQN_ERR_DEVICE, SQN_ERR_UNSUPPORTED = range(5)
 SQN_F32, SQN_F16 = 0, 1
 
-EXPORTS = ("sqn_create_caches", "sqn_render", "sqn_render_stats", "sqn_set_lanes_per_ray",
-           "sqn_set_empty_space_skipping", "sqn_cache_device_bytes", "sqn_destroy",
-           "sqn_status_string", "sqn_last_error")
+EXPORTS = ("sqn_create_caches", "sqn_create_linear_caches", "sqn_render", "sqn_render_stats",
+           "sqn_set_lanes_per_ray", "sqn_set_empty_space_skipping", "sqn_cache_device_bytes",
+           "sqn_destroy", "sqn_status_string", "sqn_last_error")
 
 
 class CacheDesc(ctypes.Structure):
@@ -31,6 +31,12 @@ class CacheDesc(ctypes.Structure):
                 ("bbox_min", ctypes.c_float * 3), ("bbox_max", ctypes.c_float * 3),
                 ("t_eps", ctypes.c_float), ("reserved", ctypes.c_int32),
                 ("seed", ctypes.c_uint64)]
+
+
+class LinearDecoder(ctypes.Structure):
+    _fields_ = [("d_sigma", ctypes.c_int32), ("b_sigma", ctypes.c_float),
+                ("w_sigma", ctypes.c_void_p), ("w_uvw", ctypes.c_void_p),
+                ("b_uvw", ctypes.c_void_p)]
 
 
 class Intrinsics(ctypes.Structure):
@@ -55,6 +61,10 @@ def _load() -> ctypes.CDLL:
     lib.sqn_create_caches.restype = ctypes.c_int
     lib.sqn_create_caches.argtypes = [ctypes.POINTER(CacheDesc), ctypes.POINTER(vp),
                                       ctypes.POINTER(vp), vp, vp, ctypes.POINTER(vp)]
+    lib.sqn_create_linear_caches.restype = ctypes.c_int
+    lib.sqn_create_linear_caches.argtypes = [ctypes.POINTER(CacheDesc), ctypes.POINTER(LinearDecoder),
+                                             ctypes.POINTER(vp), ctypes.POINTER(vp), vp, vp,
+                                             ctypes.POINTER(vp)]
     lib.sqn_render.restype = ctypes.c_int
     lib.sqn_render.argtypes = [vp, vp, i32, ctypes.POINTER(Intrinsics), f32, f32, i32, vp, vp, vp]
     lib.sqn_render_stats.restype = ctypes.c_int
@@ -115,11 +125,14 @@ def _intrinsics(intr: dict) -> Intrinsics:
 
 
 class Caches:
-    """Library-owned device copy of the SqueezeNeRF caches (sqn_create_caches)."""
+    """Library-owned device copy of the SqueezeNeRF caches (sqn_create_caches,
+    or sqn_create_linear_caches when `decoder` is given: an object with
+    w_sigma [3 D_sigma], b_sigma, w_uvw [3][D][3D] and b_uvw [3][D], and
+    sigma planes of shape [n_p][n_p][D_sigma])."""
 
     def __init__(self, sigma: Sequence[torch.Tensor], uvw: Sequence[torch.Tensor],
                  beta: torch.Tensor, bbox_min, bbox_max, t_eps: float = 1e-4,
-                 stratified: bool = False, seed: int = 0, stream=None):
+                 stratified: bool = False, seed: int = 0, stream=None, decoder=None):
         self._h = ctypes.c_void_p(None)
         sigma = [s.contiguous() for s in sigma]
         uvw = [u.contiguous() for u in uvw]
@@ -141,8 +154,24 @@ class Caches:
         self.desc = desc
         sp = (ctypes.c_void_p * 3)(*[s.data_ptr() for s in sigma])
         up = (ctypes.c_void_p * 3)(*[u.data_ptr() for u in uvw])
-        _check(lib.sqn_create_caches(ctypes.byref(desc), sp, up, _ptr(beta), _stream(stream),
-                                     ctypes.byref(self._h)))
+        if decoder is None:
+            _check(lib.sqn_create_caches(ctypes.byref(desc), sp, up, _ptr(beta), _stream(stream),
+                                         ctypes.byref(self._h)))
+            return
+        import numpy as np
+        w_sigma = np.ascontiguousarray(decoder.w_sigma, dtype=np.float32)
+        w_uvw = np.ascontiguousarray(decoder.w_uvw, dtype=np.float32)
+        b_uvw = np.ascontiguousarray(decoder.b_uvw, dtype=np.float32)
+        d_sigma = int(sigma[0].shape[2]) if sigma[0].dim() == 3 else 0
+        # the library reads these host arrays at these sizes
+        if (w_sigma.shape != (3 * d_sigma,) or w_uvw.shape != (3, D, 3 * D)
+                or b_uvw.shape != (3, D)):
+            raise ValueError("decoder weights do not match d_sigma and D")
+        dec = LinearDecoder(d_sigma,
+                            float(decoder.b_sigma), w_sigma.ctypes.data, w_uvw.ctypes.data,
+                            b_uvw.ctypes.data)
+        _check(lib.sqn_create_linear_caches(ctypes.byref(desc), ctypes.byref(dec), sp, up,
+                                            _ptr(beta), _stream(stream), ctypes.byref(self._h)))
 
     @property
     def handle(self) -> ctypes.c_void_p:
@@ -216,5 +245,5 @@ def caches_from_scene(scene, device="cuda", t_eps=None, stratified=None, stream=
     caches = Caches(sig, uvw, beta, scene.bbox_min, scene.bbox_max,
                     t_eps=cfg.t_eps if t_eps is None else t_eps,
                     stratified=cfg.stratified if stratified is None else stratified,
-                    seed=scene.seed, stream=stream)
+                    seed=scene.seed, stream=stream, decoder=getattr(scene, "decoder", None))
     return caches

@@ -9,6 +9,7 @@
 
 #include <limits>
 #include <string>
+#include <vector>
 
 #include "sqn_internal.h"
 
@@ -24,6 +25,11 @@ struct sqn_caches {
     int64_t tau_eps;         // floor(-ln(eps) 2^32)
     int32_t lanes;           // lanes per ray, 0 = chosen per call
     int32_t skip;            // empty-space leaps (one lane per ray)
+    // linear (Eq. 5) decoder
+    int32_t linear;          // 1: sigma[j] hold per-plane partial sums
+    int32_t d_sigma;
+    float b_sigma;
+    const float* lin_w;      // [9D + 3][D] folded radiance weights and biases
 };
 
 namespace {
@@ -166,6 +172,28 @@ sqn_status validate_render(const sqn_caches* h, const float* poses, int32_t n_po
     return SQN_OK;
 }
 
+sqn_status validate_decoder(const sqn_linear_decoder* dec, int32_t D)
+{
+    if (!dec)
+        return fail(SQN_ERR_INVALID_ARG, "decoder is NULL");
+    if (dec->d_sigma < 1 || dec->d_sigma > 64)
+        return fail(SQN_ERR_INVALID_ARG, "d_sigma = %d outside [1, 64]", dec->d_sigma);
+    if (!dec->w_sigma || !dec->w_uvw || !dec->b_uvw)
+        return fail(SQN_ERR_INVALID_ARG, "decoder weight pointer is NULL");
+    if (!isfinite(dec->b_sigma))
+        return fail(SQN_ERR_INVALID_ARG, "b_sigma is not finite");
+    for (int32_t k = 0; k < 3 * dec->d_sigma; ++k)
+        if (!isfinite(dec->w_sigma[k]))
+            return fail(SQN_ERR_INVALID_ARG, "w_sigma[%d] is not finite", k);
+    for (int32_t k = 0; k < 9 * D * D; ++k)
+        if (!isfinite(dec->w_uvw[k]))
+            return fail(SQN_ERR_INVALID_ARG, "w_uvw[%d] is not finite", k);
+    for (int32_t k = 0; k < 3 * D; ++k)
+        if (!isfinite(dec->b_uvw[k]))
+            return fail(SQN_ERR_INVALID_ARG, "b_uvw[%d] is not finite", k);
+    return SQN_OK;
+}
+
 // Lanes per ray for a call of `rays` rays.  One lane per ray does the least
 // work per sample, but a wave lives as long as its longest ray: below about
 // 2^20 rays (one 800x800 view is 10^4 waves against 8192 resident wave
@@ -229,7 +257,14 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
     p.inv_dt = 1.0f / p.dt;
     const int64_t rays = static_cast<int64_t>(n_poses) * in->width * in->height;
     p.skip = h->skip;
-    p.lanes = h->lanes != 0 ? h->lanes : choose_lanes(rays);
+    // the folded Eq. 5 weights are shared by the lanes of a ray in LDS, which
+    // holds them for 64 rays per workgroup, i.e. four lanes per ray
+    p.lanes = h->linear ? 4 : (h->lanes != 0 ? h->lanes : choose_lanes(rays));
+    p.linear = h->linear;
+    p.b_sigma = h->b_sigma;
+    p.lin_w = h->lin_w;
+    // rows per ray in LDS; the kernels for D = 8 and 16 use lin_stride(D)
+    p.lin_stride = sqn::lin_stride_generic(h->desc.D);
     p.leap_margin = 1e-3f;
     const int tw = sqn::kTileW(p.lanes), th = sqn::kTileH(p.lanes);
     p.tiles_x = (in->width + tw - 1) / tw;
@@ -239,20 +274,19 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
         return fail(SQN_ERR_INVALID_ARG, "too many workgroups (%lld)", static_cast<long long>(groups));
     p.n_groups = static_cast<int32_t>(groups);
 
-    hipError_t e = sqn::launch_render(p, h->desc.sigma_dtype, h->desc.uvw_dtype, with_stats,
+    // the linear decoder's records hold binary32 partial sums
+    const int sigma_records = h->linear ? SQN_F32 : h->desc.sigma_dtype;
+    hipError_t e = sqn::launch_render(p, sigma_records, h->desc.uvw_dtype, with_stats,
                                       static_cast<hipStream_t>(stream));
     if (e != hipSuccess)
         return fail(SQN_ERR_DEVICE, "render launch failed: %s", hipGetErrorString(e));
     return SQN_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-sqn_status sqn_create_caches(const sqn_cache_desc* desc, const void* const sigma_planes[3],
-                             const void* const uvw_planes[3], const void* beta, void* stream,
-                             sqn_caches** out)
+// Shared body of the two create calls; dec == NULL selects Eq. 4.
+sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec,
+                       const void* const sigma_planes[3], const void* const uvw_planes[3],
+                       const void* beta, void* stream, sqn_caches** out)
 {
     if (!out)
         return fail(SQN_ERR_INVALID_ARG, "out is NULL");
@@ -260,16 +294,24 @@ sqn_status sqn_create_caches(const sqn_cache_desc* desc, const void* const sigma
     sqn_status s = validate_desc(desc);
     if (s != SQN_OK)
         return s;
+    const bool linear = dec != nullptr;
+    if (linear && (s = validate_decoder(dec, desc->D)) != SQN_OK)
+        return s;
     if (!sigma_planes || !uvw_planes)
         return fail(SQN_ERR_INVALID_ARG, "plane pointer array is NULL");
 
+    const int32_t D = desc->D;
+    const int32_t ds = linear ? dec->d_sigma : 1;
     const size_t texels = static_cast<size_t>(desc->n_p) * desc->n_p;
-    const size_t sigma_bytes = texels * dtype_size(desc->sigma_dtype);
-    // packed (sigma, distance) records: 4 bytes for binary16 sigma, 8 for binary32
-    const size_t packed_bytes = texels * (desc->sigma_dtype == SQN_F16 ? 4 : 8);
-    const size_t uvw_bytes = texels * 3 * desc->D * dtype_size(desc->uvw_dtype);
-    const size_t beta_bytes = static_cast<size_t>(desc->n_theta) * desc->n_phi * desc->D
+    const size_t sigma_bytes = texels * ds * dtype_size(desc->sigma_dtype);
+    // packed records: 4 bytes for binary16 sigma, 8 for binary32 sigma or
+    // the linear decoder's binary32 partial sums
+    const size_t packed_bytes = texels * (!linear && desc->sigma_dtype == SQN_F16 ? 4 : 8);
+    const size_t uvw_bytes = texels * 3 * D * dtype_size(desc->uvw_dtype);
+    const size_t beta_bytes = static_cast<size_t>(desc->n_theta) * desc->n_phi * D
                               * dtype_size(desc->beta_dtype);
+    const size_t lin_rows = 9 * static_cast<size_t>(D) + 3;
+    const size_t lin_bytes = linear ? lin_rows * D * sizeof(float) : 0;
     static const char* names_s[3] = {"sigma_planes[0] (xy)", "sigma_planes[1] (yz)", "sigma_planes[2] (zx)"};
     static const char* names_u[3] = {"uvw_planes[0] (xy)", "uvw_planes[1] (yz)", "uvw_planes[2] (zx)"};
     for (int j = 0; j < 3; ++j) {
@@ -282,7 +324,7 @@ sqn_status sqn_create_caches(const sqn_cache_desc* desc, const void* const sigma
         return s;
 
     auto align = [](size_t x) { return (x + 255) & ~size_t{255}; };
-    size_t off_sigma[3], off_uvw[3], off_beta, total = 0;
+    size_t off_sigma[3], off_uvw[3], off_beta, off_lin, total = 0;
     for (int j = 0; j < 3; ++j) {
         off_sigma[j] = total;
         total += align(packed_bytes);
@@ -293,6 +335,38 @@ sqn_status sqn_create_caches(const sqn_cache_desc* desc, const void* const sigma
     }
     off_beta = total;
     total += align(beta_bytes);
+    off_lin = total;
+    total += align(lin_bytes);
+
+    // temporary buffers of the preparation, freed before returning
+    size_t work_total = 0;
+    const size_t w_live = work_total;
+    work_total += align(texels);
+    const size_t w_f = work_total;
+    work_total += align(texels * sizeof(uint16_t));
+    const size_t w_dist = work_total;
+    work_total += align(texels * sizeof(uint16_t));
+    const size_t w_max = work_total;
+    work_total += align(6 * static_cast<size_t>(desc->n_p) * sizeof(float));
+    const size_t w_ws = work_total;
+    work_total += align(3 * static_cast<size_t>(ds) * sizeof(float));
+
+    // host-side parameters of the linear decoder: W_sigma, and the radiance
+    // weights transposed so that row c*3D + e holds W_c[0..D)[e], followed
+    // by the rows b_u, b_v, b_w
+    std::vector<float> lin_host, ws_host;
+    if (linear) {
+        lin_host.resize(lin_rows * D);
+        for (int32_t c = 0; c < 3; ++c)
+            for (int32_t e = 0; e < 3 * D; ++e)
+                for (int32_t d = 0; d < D; ++d)
+                    lin_host[(static_cast<size_t>(c) * 3 * D + e) * D + d]
+                        = dec->w_uvw[(static_cast<size_t>(c) * D + d) * 3 * D + e];
+        for (int32_t c = 0; c < 3; ++c)
+            for (int32_t d = 0; d < D; ++d)
+                lin_host[(9 * static_cast<size_t>(D) + c) * D + d] = dec->b_uvw[c * D + d];
+        ws_host.assign(dec->w_sigma, dec->w_sigma + 3 * ds);
+    }
 
     sqn_caches* h = static_cast<sqn_caches*>(calloc(1, sizeof(sqn_caches)));
     if (!h)
@@ -315,28 +389,48 @@ sqn_status sqn_create_caches(const sqn_cache_desc* desc, const void* const sigma
     h->bytes = total;
     char* base = static_cast<char*>(h->block);
     hipStream_t st = static_cast<hipStream_t>(stream);
-    // scratch for the distance transform, freed before returning
-    uint16_t* work = nullptr;
-    e = hipMalloc(reinterpret_cast<void**>(&work), 2 * texels * sizeof(uint16_t));
+    char* work = nullptr;
+    e = hipMalloc(reinterpret_cast<void**>(&work), work_total);
     if (e != hipSuccess) {
         (void)hipGetLastError();
         (void)hipFree(h->block);
         free(h);
-        return fail(SQN_ERR_OUT_OF_MEMORY, "hipMalloc of %zu scratch bytes failed", 2 * texels * sizeof(uint16_t));
+        return fail(SQN_ERR_OUT_OF_MEMORY, "hipMalloc of %zu scratch bytes failed", work_total);
     }
-    for (int j = 0; j < 3 && e == hipSuccess; ++j) {
-        h->sigma[j] = base + off_sigma[j];
+    sqn::PrepareWork pw;
+    pw.live = reinterpret_cast<uint8_t*>(work + w_live);
+    pw.f = reinterpret_cast<uint16_t*>(work + w_f);
+    pw.dist = reinterpret_cast<uint16_t*>(work + w_dist);
+    pw.maxima = reinterpret_cast<float*>(work + w_max);
+    pw.w_sigma = reinterpret_cast<float*>(work + w_ws);
+
+    void* packed[3];
+    for (int j = 0; j < 3; ++j) {
+        packed[j] = base + off_sigma[j];
+        h->sigma[j] = packed[j];
         h->uvw[j] = base + off_uvw[j];
-        e = sqn::prepare_sigma_plane(sigma_planes[j], desc->sigma_dtype, desc->n_p, base + off_sigma[j],
-                                     work, work + texels, st);
-        if (e == hipSuccess)
-            e = hipMemcpyAsync(base + off_uvw[j], uvw_planes[j], uvw_bytes, hipMemcpyDeviceToDevice, st);
     }
     h->beta = base + off_beta;
+    if (linear) {
+        e = hipMemcpyAsync(pw.w_sigma, ws_host.data(), ws_host.size() * sizeof(float),
+                           hipMemcpyHostToDevice, st);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(base + off_lin, lin_host.data(), lin_bytes, hipMemcpyHostToDevice, st);
+        if (e == hipSuccess)
+            e = sqn::prepare_linear_planes(sigma_planes, desc->sigma_dtype, desc->n_p, ds, dec->b_sigma,
+                                           packed, pw, st);
+    } else {
+        for (int j = 0; j < 3 && e == hipSuccess; ++j)
+            e = sqn::prepare_sigma_plane(sigma_planes[j], desc->sigma_dtype, desc->n_p, packed[j], pw, st);
+    }
+    for (int j = 0; j < 3 && e == hipSuccess; ++j)
+        e = hipMemcpyAsync(base + off_uvw[j], uvw_planes[j], uvw_bytes, hipMemcpyDeviceToDevice, st);
     if (e == hipSuccess)
         e = hipMemcpyAsync(base + off_beta, beta, beta_bytes, hipMemcpyDeviceToDevice, st);
     if (e == hipSuccess)
         e = hipStreamSynchronize(st);
+    else
+        (void)hipStreamSynchronize(st);
     (void)hipFree(work);
     if (e != hipSuccess) {
         (void)hipGetLastError();
@@ -348,9 +442,38 @@ sqn_status sqn_create_caches(const sqn_cache_desc* desc, const void* const sigma
         h->scale[r] = static_cast<float>(desc->n_p - 1) / (desc->bbox_max[r] - desc->bbox_min[r]);
     h->tau_eps = tau_threshold(desc->t_eps);
     h->skip = 1;
+    if (linear) {
+        h->linear = 1;
+        h->d_sigma = ds;
+        h->b_sigma = dec->b_sigma;
+        h->lin_w = reinterpret_cast<const float*>(base + off_lin);
+    }
     *out = h;
     g_last_error.clear();
     return SQN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sqn_status sqn_create_caches(const sqn_cache_desc* desc, const void* const sigma_planes[3],
+                             const void* const uvw_planes[3], const void* beta, void* stream,
+                             sqn_caches** out)
+{
+    return create_impl(desc, nullptr, sigma_planes, uvw_planes, beta, stream, out);
+}
+
+sqn_status sqn_create_linear_caches(const sqn_cache_desc* desc, const sqn_linear_decoder* decoder,
+                                    const void* const sigma_planes[3], const void* const uvw_planes[3],
+                                    const void* beta, void* stream, sqn_caches** out)
+{
+    if (!decoder) {
+        if (out)
+            *out = nullptr;
+        return fail(SQN_ERR_INVALID_ARG, "decoder is NULL");
+    }
+    return create_impl(desc, decoder, sigma_planes, uvw_planes, beta, stream, out);
 }
 
 sqn_status sqn_render(const sqn_caches* caches, const float* poses, int32_t n_poses,
@@ -388,6 +511,8 @@ sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes)
         return fail(SQN_ERR_INVALID_ARG, "caches is NULL");
     if (lanes != 0 && lanes != 1 && lanes != 4)
         return fail(SQN_ERR_INVALID_ARG, "lanes per ray must be 0, 1 or 4 (got %d)", lanes);
+    if (caches->linear && lanes == 1)
+        return fail(SQN_ERR_UNSUPPORTED, "the linear decoder renders with four lanes per ray");
     caches->lanes = lanes;
     return SQN_OK;
 }

@@ -1,32 +1,49 @@
-// Create-time preparation of the position planes: for each plane j the
-// Chebyshev (L-infinity) distance, in texels, from every texel to the
-// nearest texel with sigma^j != 0, capped at kDistCap, packed next to sigma^j.
+// Create-time preparation of the position planes: for each plane j a mask of
+// the texels whose samples may have sigma > 0, the Chebyshev (L-infinity)
+// distance in texels from every texel to the nearest such texel (capped at
+// kDistCap), and a record that packs the distance next to the value the
+// render kernel reads.
 //
-// sigma = sigma^xy sigma^yz sigma^zx (Eq. 4) vanishes wherever one factor
-// does, so a sample whose plane-j texel has distance D > 0 is empty, and so
-// is every sample whose plane-j texel stays within Chebyshev distance D - 1
-// of it: the render kernel leaps over such runs.  A texel counts as
-// occupied unless its stored value compares equal to zero (NaN counts as
-// occupied), so distances never overstate the empty space.
+// Eq. 4: sigma = sigma^xy sigma^yz sigma^zx vanishes wherever one factor
+// does, so a texel is live unless its sigma^j compares equal to zero (NaN
+// counts as live).
 //
-// L-infinity distance is separable: with f(a, b) the distance along row a
-// from column b to the nearest occupied texel of that row,
-//   dist(a, b) = min over a' of max(|a - a'|, f(a', b)).
+// Eq. 5 (linear decoder): sigma = max(0, W_sigma concat(sigma^j) + b_sigma)
+// is evaluated as ((s^xy + s^yz) + s^zx) + b_sigma from per-plane partial
+// sums s^j (a chain of fused multiply-adds over the channels of plane j).
+// The partial sums are folded here, once, into the records.  A texel of plane
+// j is dead when the same expression with the other two partial sums replaced
+// by their maxima over the samples that can share this texel (a row or column
+// of the other planes) is <= 0: binary32 addition is monotone, so every such
+// sample then has a sum <= 0 or NaN, i.e. sigma = 0.
+//
+// A sample whose plane-j texel has distance D > 0 is empty, and so is every
+// sample whose plane-j texel stays within Chebyshev distance D - 1 of it: the
+// render kernel leaps over such runs.  L-infinity distance is separable: with
+// f(a, b) the distance along row a from column b to the nearest live texel of
+// that row, dist(a, b) = min over a' of max(|a - a'|, f(a', b)).
+#include <math.h>
+
 #include "sqn_internal.h"
 
 namespace sqn {
 namespace {
 
+__device__ __forceinline__ float widen(float x) { return x; }
+__device__ __forceinline__ float widen(_Float16 x) { return static_cast<float>(x); }
+
+// Eq. 4 planes: live unless sigma^j == 0.
 template <typename ST>
-__device__ __forceinline__ bool occupied(const ST* plane, uint32_t idx)
+__global__ void nonzero_mask(const ST* __restrict__ plane, uint8_t* __restrict__ live, uint32_t n)
 {
-    return !(static_cast<float>(plane[idx]) == 0.0f);
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n)
+        live[i] = (static_cast<float>(plane[i]) == 0.0f) ? 0 : 1;
 }
 
 // One thread per row: forward and backward sweeps give the distance along
-// the row to the nearest occupied texel, capped at cap + 1.
-template <typename ST>
-__global__ void row_distance(const ST* __restrict__ plane, uint16_t* __restrict__ f, int32_t n_p,
+// the row to the nearest live texel, capped at cap + 1.
+__global__ void row_distance(const uint8_t* __restrict__ live, uint16_t* __restrict__ f, int32_t n_p,
                              int32_t cap)
 {
     const int32_t a = blockIdx.x * blockDim.x + threadIdx.x;
@@ -36,13 +53,13 @@ __global__ void row_distance(const ST* __restrict__ plane, uint16_t* __restrict_
     const int32_t far = cap + 1;
     int32_t last = -(1 << 30);
     for (int32_t b = 0; b < n_p; ++b) {
-        if (occupied(plane, row + b))
+        if (live[row + b])
             last = b;
         f[row + b] = static_cast<uint16_t>(min(far, b - last));
     }
     last = 1 << 30;
     for (int32_t b = n_p - 1; b >= 0; --b) {
-        if (occupied(plane, row + b))
+        if (live[row + b])
             last = b;
         const int32_t fb = min(far, last - b);
         if (fb < f[row + b])
@@ -86,32 +103,176 @@ __global__ void pack_f32(const uint32_t* __restrict__ sigma, const uint16_t* __r
         out[i] = make_uint2(sigma[i], static_cast<uint32_t>(dist[i]));
 }
 
-}  // namespace
-
-hipError_t prepare_sigma_plane(const void* sigma, int sigma_dtype, int32_t n_p, void* packed,
-                               uint16_t* work_f, uint16_t* work_dist, hipStream_t stream)
+// Distance and packing of one plane whose live mask is in work.live.
+hipError_t distance_transform(int32_t n_p, const PrepareWork& work, hipStream_t stream)
 {
-    const uint32_t n = static_cast<uint32_t>(n_p) * static_cast<uint32_t>(n_p);
     const int32_t cap = kDistCap;
-    const dim3 rows((n_p + 63) / 64);
-    if (sigma_dtype == SQN_F16)
-        row_distance<_Float16><<<rows, 64, 0, stream>>>(static_cast<const _Float16*>(sigma), work_f, n_p, cap);
-    else
-        row_distance<float><<<rows, 64, 0, stream>>>(static_cast<const float*>(sigma), work_f, n_p, cap);
+    row_distance<<<dim3((n_p + 63) / 64), 64, 0, stream>>>(work.live, work.f, n_p, cap);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    column_distance<<<dim3((n_p + 255) / 256, n_p), 256, 0, stream>>>(work_f, work_dist, n_p, cap);
-    if ((e = hipGetLastError()) != hipSuccess)
-        return e;
+    column_distance<<<dim3((n_p + 255) / 256, n_p), 256, 0, stream>>>(work.f, work.dist, n_p, cap);
+    return hipGetLastError();
+}
+
+// ---- linear decoder -------------------------------------------------------
+
+// s^j at every texel: fma chain over the d_sigma channels from zero, in
+// channel order (the evaluation order of the density, see the file head).
+template <typename ST>
+__global__ void fold_partials(const ST* __restrict__ sigma, const float* __restrict__ w, int32_t ds,
+                              uint2* __restrict__ packed, uint32_t n)
+{
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n)
+        return;
+    const ST* v = sigma + static_cast<size_t>(i) * static_cast<size_t>(ds);
+    float s = 0.0f;
+    for (int32_t c = 0; c < ds; ++c)
+        s = __builtin_fmaf(w[c], widen(v[c]), s);
+    packed[i] = make_uint2(__float_as_uint(s), 0u);
+}
+
+// max over b of s[a][b] for each row a (one workgroup per row).  fmaxf skips
+// NaN, whose samples have zero density anyway; an all-NaN row gives -inf.
+__global__ void row_max(const uint2* __restrict__ packed, float* __restrict__ out, int32_t n_p)
+{
+    __shared__ float part[256];
+    const int32_t a = blockIdx.x;
+    const uint32_t row = static_cast<uint32_t>(a) * static_cast<uint32_t>(n_p);
+    float m = -INFINITY;
+    for (int32_t b = threadIdx.x; b < n_p; b += blockDim.x)
+        m = fmaxf(m, __uint_as_float(packed[row + b].x));
+    part[threadIdx.x] = m;
+    __syncthreads();
+    for (int32_t k = blockDim.x / 2; k > 0; k >>= 1) {
+        if (static_cast<int32_t>(threadIdx.x) < k)
+            part[threadIdx.x] = fmaxf(part[threadIdx.x], part[threadIdx.x + k]);
+        __syncthreads();
+    }
+    if (threadIdx.x == 0)
+        out[a] = part[0];
+}
+
+// max over a of s[a][b] for each column b (one thread per column).
+__global__ void col_max(const uint2* __restrict__ packed, float* __restrict__ out, int32_t n_p)
+{
+    const int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= n_p)
+        return;
+    float m = -INFINITY;
+    for (int32_t a = 0; a < n_p; ++a)
+        m = fmaxf(m, __uint_as_float(packed[static_cast<uint32_t>(a) * n_p + b].x));
+    out[b] = m;
+}
+
+// Live mask of plane j.  maxima[2k] / maxima[2k + 1] are the row / column
+// maxima of plane k (planes xy = [x][y], yz = [y][z], zx = [z][x]); the
+// texel (a, b) of plane j shares samples with
+//   xy (x=a, y=b): s^yz over row y, s^zx over column x
+//   yz (y=a, z=b): s^xy over column y, s^zx over row z
+//   zx (z=a, x=b): s^xy over row x, s^yz over column z
+// and the bound keeps the evaluation order ((s^xy + s^yz) + s^zx) + b.
+__global__ void linear_live(const uint2* __restrict__ packed, const float* __restrict__ maxima, int32_t j,
+                            int32_t n_p, float b_sigma, uint8_t* __restrict__ live)
+{
+    const int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
+    const int32_t a = blockIdx.y;
+    if (b >= n_p)
+        return;
+    const uint32_t i = static_cast<uint32_t>(a) * static_cast<uint32_t>(n_p) + b;
+    const float s = __uint_as_float(packed[i].x);
+    const float* m = maxima;
+    float s_xy, s_yz, s_zx;
+    if (j == 0) {
+        s_xy = s;
+        s_yz = m[2 * n_p + b];
+        s_zx = m[5 * n_p + a];
+    } else if (j == 1) {
+        s_xy = m[1 * n_p + a];
+        s_yz = s;
+        s_zx = m[4 * n_p + b];
+    } else {
+        s_xy = m[0 * n_p + b];
+        s_yz = m[3 * n_p + a];
+        s_zx = s;
+    }
+    float bound = s_xy + s_yz;
+    bound = bound + s_zx;
+    bound = bound + b_sigma;
+    live[i] = (bound <= 0.0f) ? 0 : 1;
+}
+
+__global__ void set_distance(const uint16_t* __restrict__ dist, uint2* __restrict__ packed, uint32_t n)
+{
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n)
+        packed[i].y = static_cast<uint32_t>(dist[i]);
+}
+
+}  // namespace
+
+hipError_t prepare_sigma_plane(const void* sigma, int sigma_dtype, int32_t n_p, void* packed,
+                               const PrepareWork& work, hipStream_t stream)
+{
+    const uint32_t n = static_cast<uint32_t>(n_p) * static_cast<uint32_t>(n_p);
     const dim3 grid((n + 255) / 256);
     if (sigma_dtype == SQN_F16)
-        pack_f16<<<grid, 256, 0, stream>>>(static_cast<const uint16_t*>(sigma), work_dist,
+        nonzero_mask<_Float16><<<grid, 256, 0, stream>>>(static_cast<const _Float16*>(sigma), work.live, n);
+    else
+        nonzero_mask<float><<<grid, 256, 0, stream>>>(static_cast<const float*>(sigma), work.live, n);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    if ((e = distance_transform(n_p, work, stream)) != hipSuccess)
+        return e;
+    if (sigma_dtype == SQN_F16)
+        pack_f16<<<grid, 256, 0, stream>>>(static_cast<const uint16_t*>(sigma), work.dist,
                                            static_cast<uint32_t*>(packed), n);
     else
-        pack_f32<<<grid, 256, 0, stream>>>(static_cast<const uint32_t*>(sigma), work_dist,
+        pack_f32<<<grid, 256, 0, stream>>>(static_cast<const uint32_t*>(sigma), work.dist,
                                            static_cast<uint2*>(packed), n);
     return hipGetLastError();
+}
+
+hipError_t prepare_linear_planes(const void* const sigma[3], int sigma_dtype, int32_t n_p,
+                                 int32_t d_sigma, float b_sigma, void* const packed[3],
+                                 const PrepareWork& work, hipStream_t stream)
+{
+    const uint32_t n = static_cast<uint32_t>(n_p) * static_cast<uint32_t>(n_p);
+    const dim3 grid((n + 255) / 256);
+    hipError_t e = hipSuccess;
+    for (int j = 0; j < 3; ++j) {
+        uint2* rec = static_cast<uint2*>(packed[j]);
+        const float* w = work.w_sigma + j * d_sigma;
+        if (sigma_dtype == SQN_F16)
+            fold_partials<_Float16><<<grid, 256, 0, stream>>>(static_cast<const _Float16*>(sigma[j]), w,
+                                                              d_sigma, rec, n);
+        else
+            fold_partials<float><<<grid, 256, 0, stream>>>(static_cast<const float*>(sigma[j]), w, d_sigma,
+                                                           rec, n);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+        row_max<<<dim3(n_p), 256, 0, stream>>>(rec, work.maxima + (2 * j) * n_p, n_p);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+        col_max<<<dim3((n_p + 255) / 256), 256, 0, stream>>>(rec, work.maxima + (2 * j + 1) * n_p, n_p);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+    }
+    for (int j = 0; j < 3; ++j) {
+        uint2* rec = static_cast<uint2*>(packed[j]);
+        linear_live<<<dim3((n_p + 255) / 256, n_p), 256, 0, stream>>>(rec, work.maxima, j, n_p, b_sigma,
+                                                                      work.live);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+        if ((e = distance_transform(n_p, work, stream)) != hipSuccess)
+            return e;
+        set_distance<<<grid, 256, 0, stream>>>(work.dist, rec, n);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace sqn

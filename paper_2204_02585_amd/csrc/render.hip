@@ -12,7 +12,8 @@
 // Per ray: pinhole ray (Sec. 3.1); a conservative clip of the sample range to
 // the scene box (samples outside it have sigma = 0 and add nothing); the
 // bilinear direction lookup of beta (Sec. 3.4).  Per sample: nearest-node
-// gathers of the three sigma^j and their product (Eq. 4); the 2^-32
+// gathers of the three sigma^j and their product (Eq. 4), or of the three
+// per-plane partial sums of Eq. 5 and their biased sum; the 2^-32
 // fixed-point optical depth increment, scanned exactly across the L lanes;
 // the termination test T_i >= eps (Eq. 1); and only for live samples with
 // sigma > 0 the three uvw records, beta^T (sum of the planar uvw) (Eq. 4 and
@@ -273,7 +274,7 @@ __device__ __forceinline__ void clip_to_box(const RenderParams& P, const float o
 // L >= 2 the even lanes of the group evaluate theta and the odd lanes phi,
 // and each lane weights a share of the four corner texels before a group
 // sum.
-template <int DC, int L>
+template <int DC, int L, int BS>
 __device__ __forceinline__ void lookup_beta(const RenderParams& P, const float d[3], int s,
                                             float* beta_lds)
 {
@@ -326,13 +327,14 @@ __device__ __forceinline__ void lookup_beta(const RenderParams& P, const float d
         }
         return grp_sum<L>(acc);
     };
+    // component k goes to beta_lds[k * BS]
     if constexpr (DC > 0) {
 #pragma unroll
         for (int k = 0; k < DC; ++k)
-            beta_lds[k * kBlockThreads] = component(k);
+            beta_lds[k * BS] = component(k);
     } else {
         for (int k = 0; k < D; ++k)
-            beta_lds[k * kBlockThreads] = component(k);
+            beta_lds[k * BS] = component(k);
     }
 }
 
@@ -386,6 +388,107 @@ __device__ __forceinline__ void sample_colour(const RenderParams& P, uint32_t t0
                 x = fmaf(bk, widen(load_at<UT>(P.uvw[1], (t1 * nv + off) * esz)), x);
                 x = fmaf(bk, widen(load_at<UT>(P.uvw[2], (t2 * nv + off) * esz)), x);
             }
+            col[c] = sigmoid(x);
+        }
+    }
+}
+
+// Eq. 5 decoder, folded into Eq. 2 once per ray: with beta fixed along the
+// ray, the logit of channel c is
+//   beta^T (W_c concat_c + b_c) = sum_e (W_c^T beta)_e concat_c[e] + beta^T b_c,
+// so each ray keeps the 9D values W_c^T beta and the three beta^T b_c (rows
+// of lin_w: c*3D + e, then the biases) and every occupied sample costs one
+// 3D-term inner product per channel, as with Eq. 4.  The L lanes of the ray
+// compute every L-th row and store it in the ray's LDS row `lin`, where beta
+// waits: in lin[0, D) for a compile-time D (read into registers before any
+// row is written: LDS operations of one wavefront complete in order), else
+// in lin[9D + 3, 10D + 3).
+template <int DC, int L>
+__device__ __forceinline__ void fold_decoder(const RenderParams& P, int s, float* lin)
+{
+    if constexpr (DC > 0) {
+        constexpr int32_t rows = 9 * DC + 3;
+        float b[DC];
+#pragma unroll
+        for (int k = 0; k < DC; ++k)
+            b[k] = lin[k];
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        for (int32_t o = s; o < rows; o += L) {
+            const float4* w = reinterpret_cast<const float4*>(P.lin_w + o * DC);
+            float acc = 0.0f;
+#pragma unroll
+            for (int k = 0; k < DC / 4; ++k) {
+                const float4 w4 = w[k];
+                acc = fmaf(b[4 * k + 0], w4.x, acc);
+                acc = fmaf(b[4 * k + 1], w4.y, acc);
+                acc = fmaf(b[4 * k + 2], w4.z, acc);
+                acc = fmaf(b[4 * k + 3], w4.w, acc);
+            }
+            lin[o] = acc;
+        }
+    } else {
+        const int32_t D = P.D;
+        const int32_t rows = 9 * D + 3;
+        for (int32_t o = s; o < rows; o += L) {
+            const float* w = P.lin_w + o * D;
+            float acc = 0.0f;
+            for (int32_t k = 0; k < D; ++k)
+                acc = fmaf(lin[rows + k], w[k], acc);
+            lin[o] = acc;
+        }
+    }
+    // the other lanes of the ray (same wavefront) read these rows; LDS
+    // operations of one wavefront complete in order, so ordering the code
+    // suffices
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Colour of one occupied sample under Eq. 5: per channel c,
+// sigmoid(beta^T b_c + sum_j sum_e (W_c^T beta)[jD + e] k^j_c[e]).
+template <typename UT, int DC>
+__device__ __forceinline__ void sample_colour_lin(const RenderParams& P, uint32_t t0, uint32_t t1,
+                                                  uint32_t t2, const float* lin, float col[3])
+{
+    const uint32_t texel[3] = {t0, t1, t2};
+    if constexpr (DC > 0 && DC % 4 == 0 && (3 * DC * sizeof(UT)) % 16 == 0) {
+        constexpr int NV = 3 * DC;
+        constexpr uint32_t NB = NV * static_cast<uint32_t>(sizeof(UT));
+        constexpr int NQ = NB / 16;
+        float x[3] = {lin[9 * DC + 0], lin[9 * DC + 1], lin[9 * DC + 2]};
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+            uint4 q[NQ];
+#pragma unroll
+            for (int k = 0; k < NQ; ++k)
+                q[k] = load_at<uint4>(P.uvw[j], texel[j] * NB + 16u * k);
+            UT rec[NV];
+            __builtin_memcpy(rec, q, NB);
+#pragma unroll
+            for (int c = 0; c < 3; ++c)
+#pragma unroll
+                for (int e = 0; e < DC; e += 4) {
+                    const float4 w = *reinterpret_cast<const float4*>(lin + c * 3 * DC + j * DC + e);
+                    x[c] = fmaf(w.x, widen(rec[c * DC + e + 0]), x[c]);
+                    x[c] = fmaf(w.y, widen(rec[c * DC + e + 1]), x[c]);
+                    x[c] = fmaf(w.z, widen(rec[c * DC + e + 2]), x[c]);
+                    x[c] = fmaf(w.w, widen(rec[c * DC + e + 3]), x[c]);
+                }
+        }
+#pragma unroll
+        for (int c = 0; c < 3; ++c)
+            col[c] = sigmoid(x[c]);
+    } else {
+        const int32_t D = P.D;
+        const uint32_t nv = 3u * static_cast<uint32_t>(D);
+        const uint32_t esz = static_cast<uint32_t>(sizeof(UT));
+        for (int c = 0; c < 3; ++c) {
+            float x = lin[9 * D + c];
+            for (int j = 0; j < 3; ++j)
+                for (int32_t e = 0; e < D; ++e) {
+                    const uint32_t off = static_cast<uint32_t>(c * D + e);
+                    x = fmaf(lin[c * 3 * D + j * D + e], widen(load_at<UT>(P.uvw[j], (texel[j] * nv + off) * esz)), x);
+                }
             col[c] = sigmoid(x);
         }
     }
@@ -506,9 +609,9 @@ constexpr int waves_per_simd(int record_bytes)
 // SKIP: leap over runs of samples that one plane's distance field proves
 // empty (with L lanes per ray, the run that starts at the chunk's last
 // sample decides where the next chunk starts).
-template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP>
+template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool LIN>
 __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, int32_t u,
-                                           int32_t v, int32_t lane, float* const beta)
+                                           int32_t v, int32_t lane, float* const beta, float* const lin)
 {
     const int32_t s = (L == 1) ? 0 : (lane & (L - 1));
     const int64_t ray = (static_cast<int64_t>(view) * P.height + v) * P.width + u;
@@ -538,7 +641,14 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
     int32_t i0, i1;
     clip_to_box(P, o, d, i0, i1);
 
-    lookup_beta<DC, L>(P, d, s, beta);
+    if constexpr (LIN) {
+        // beta goes to the ray's LDS row (the L lanes write equal values)
+        lookup_beta<DC, L, 1>(P, d, s, DC > 0 ? lin : lin + 9 * P.D + 3);
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        fold_decoder<DC, L>(P, s, lin);
+    } else {
+        lookup_beta<DC, L, kBlockThreads>(P, d, s, beta);
+    }
 
     const int32_t n_p = P.n_p;
     const float hi_node = static_cast<float>(n_p - 1);
@@ -602,9 +712,18 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
             SigmaRecord<ST>::load(P.sigma[0], __umul24(ix, n_p) + iy, sxy, dxy);
             SigmaRecord<ST>::load(P.sigma[1], __umul24(iy, n_p) + iz, syz, dyz);
             SigmaRecord<ST>::load(P.sigma[2], __umul24(iz, n_p) + ix, szx, dzx);
-            float prod = sxy * syz;
-            prod = prod * szx;
-            sigma = fmaxf(0.0f, prod);
+            if constexpr (LIN) {
+                // Eq. 5 on the folded per-plane partial sums
+                float pre = sxy + syz;
+                pre = pre + szx;
+                pre = pre + P.b_sigma;
+                sigma = pre > 0.0f ? pre : 0.0f;
+            } else {
+                // Eq. 4
+                float prod = sxy * syz;
+                prod = prod * szx;
+                sigma = fmaxf(0.0f, prod);
+            }
             if constexpr (SKIP) {
                 const uint32_t dmax = max(dxy, max(dyz, dzx));
                 if (dmax != 0) {
@@ -658,8 +777,12 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
         const bool occ = live & (sigma > 0.0f);
         if (occ) {
             float col[3];
-            sample_colour<UT, DC>(P, __umul24(ix, n_p) + iy, __umul24(iy, n_p) + iz,
-                                  __umul24(iz, n_p) + ix, beta, col);
+            if constexpr (LIN)
+                sample_colour_lin<UT, DC>(P, __umul24(ix, n_p) + iy, __umul24(iy, n_p) + iz,
+                                          __umul24(iz, n_p) + ix, lin, col);
+            else
+                sample_colour<UT, DC>(P, __umul24(ix, n_p) + iy, __umul24(iy, n_p) + iz,
+                                      __umul24(iz, n_p) + ix, beta, col);
             const float T = transmittance(tau_i);
             const float alpha = -expm1f(-q);
             const double w = static_cast<double>(T * alpha);
@@ -742,13 +865,46 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
 
 // Launch shapes: L = 1 or 4 lanes per ray over workgroup tiles of
 // kTileW(L) x kTileH(L) pixels, with or without leaps over empty space.
-template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP>
-__global__ __launch_bounds__(kBlockThreads, waves_per_simd(3 * DC * static_cast<int>(sizeof(UT)))) void render_kernel(const RenderParams P)
+// LDS floats of the folded Eq. 5 weights per workgroup (64 rays); a run-time
+// D also keeps beta after the rows.
+template <int DC, bool LIN>
+constexpr int lin_smem_floats()
+{
+    return LIN ? (DC > 0 ? lin_stride(DC) : lin_stride_generic(32)) * (kBlockThreads / 4) : 4;
+}
+
+// LDS floats of beta per workgroup (one copy per lane; Eq. 5 keeps it in
+// the folded rows instead).
+template <int DC, bool LIN>
+constexpr int beta_smem_floats()
+{
+    return LIN ? 4 : (DC > 0 ? DC : 32) * kBlockThreads;
+}
+
+// Waves per SIMD: the register target, capped by how many 4-wave workgroups
+// the 160 KiB of LDS of a compute unit holds.
+template <typename UT, int DC, bool LIN>
+constexpr int occupancy()
+{
+    // the Eq. 5 path holds more per-ray state (LDS row pointers, folded
+    // biases); six waves leave it room without spilling
+    constexpr int rec = waves_per_simd(3 * DC * static_cast<int>(sizeof(UT)));
+    constexpr int regs = LIN && rec > 6 ? 6 : rec;
+    constexpr int lds = 4 * (lin_smem_floats<DC, LIN>() + beta_smem_floats<DC, LIN>());
+    constexpr int by_lds = 163840 / lds;
+    return regs < by_lds ? regs : (by_lds < 1 ? 1 : by_lds);
+}
+
+template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool LIN>
+__global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN>())) void render_kernel(const RenderParams P)
 {
     // beta of every lane's ray, component-major so that a wave-wide read of
     // one component touches consecutive LDS words; each lane reads only what
     // it wrote, so no barrier is needed
-    __shared__ float beta_smem[(DC > 0 ? DC : 32) * kBlockThreads];
+    __shared__ float beta_smem[beta_smem_floats<DC, LIN>()];
+    // Eq. 5: one row of folded weights per ray, written and read only by
+    // the ray's own lanes
+    __shared__ __align__(16) float lin_smem[lin_smem_floats<DC, LIN>()];
     const int32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int32_t tile = xcd_tile_order(static_cast<int32_t>(blockIdx.x), P.n_groups);
     const int32_t tiles_per_view = P.tiles_x * P.tiles_y;
@@ -761,19 +917,26 @@ __global__ __launch_bounds__(kBlockThreads, waves_per_simd(3 * DC * static_cast<
     const int32_t u = tx * kTileW(L) + (wave & 1) * WW + (slot % WW);
     const int32_t v = ty * kTileH(L) + (wave >> 1) * WH + (slot / WW);
     // all lanes of a ray agree on this, so a lane group is never split
-    if (view < P.n_views && u < P.width && v < P.height)
-        render_ray<ST, UT, DC, STATS, L, SKIP>(P, view, u, v, lane, beta_smem + threadIdx.x);
+    if (view < P.n_views && u < P.width && v < P.height) {
+        float* lin = nullptr;
+        if constexpr (LIN) {
+            constexpr int32_t stride = DC > 0 ? lin_stride(DC) : 0;
+            lin = lin_smem + (threadIdx.x / 4) * (DC > 0 ? stride : P.lin_stride);
+        }
+        render_ray<ST, UT, DC, STATS, L, SKIP, LIN>(P, view, u, v, lane,
+                                                    LIN ? beta_smem : beta_smem + threadIdx.x, lin);
+    }
 }
 
-template <typename ST, typename UT, int DC, int L, bool SKIP>
+template <typename ST, typename UT, int DC, int L, bool SKIP, bool LIN>
 hipError_t launch_shape(const RenderParams& p, bool stats, hipStream_t stream)
 {
     const dim3 grid(static_cast<uint32_t>(p.n_groups));
     const dim3 block(kBlockThreads);
     if (stats)
-        render_kernel<ST, UT, DC, true, L, SKIP><<<grid, block, 0, stream>>>(p);
+        render_kernel<ST, UT, DC, true, L, SKIP, LIN><<<grid, block, 0, stream>>>(p);
     else
-        render_kernel<ST, UT, DC, false, L, SKIP><<<grid, block, 0, stream>>>(p);
+        render_kernel<ST, UT, DC, false, L, SKIP, LIN><<<grid, block, 0, stream>>>(p);
     return hipGetLastError();
 }
 
@@ -781,10 +944,18 @@ template <typename ST, typename UT, int DC>
 hipError_t launch_typed(const RenderParams& p, bool stats, hipStream_t stream)
 {
     if (p.lanes == 1)
-        return p.skip ? launch_shape<ST, UT, DC, 1, true>(p, stats, stream)
-                      : launch_shape<ST, UT, DC, 1, false>(p, stats, stream);
-    return p.skip ? launch_shape<ST, UT, DC, 4, true>(p, stats, stream)
-                  : launch_shape<ST, UT, DC, 4, false>(p, stats, stream);
+        return p.skip ? launch_shape<ST, UT, DC, 1, true, false>(p, stats, stream)
+                      : launch_shape<ST, UT, DC, 1, false, false>(p, stats, stream);
+    return p.skip ? launch_shape<ST, UT, DC, 4, true, false>(p, stats, stream)
+                  : launch_shape<ST, UT, DC, 4, false, false>(p, stats, stream);
+}
+
+// Eq. 5: binary32 partial-sum records, four lanes per ray.
+template <typename UT, int DC>
+hipError_t launch_linear(const RenderParams& p, bool stats, hipStream_t stream)
+{
+    return p.skip ? launch_shape<float, UT, DC, 4, true, true>(p, stats, stream)
+                  : launch_shape<float, UT, DC, 4, false, true>(p, stats, stream);
 }
 
 template <typename ST, typename UT>
@@ -800,12 +971,27 @@ hipError_t launch_d(const RenderParams& p, bool stats, hipStream_t stream)
     }
 }
 
+template <typename UT>
+hipError_t launch_linear_d(const RenderParams& p, bool stats, hipStream_t stream)
+{
+    switch (p.D) {
+    case 8:
+        return launch_linear<UT, 8>(p, stats, stream);
+    case 16:
+        return launch_linear<UT, 16>(p, stats, stream);
+    default:
+        return launch_linear<UT, 0>(p, stats, stream);
+    }
+}
+
 }  // namespace
 
 hipError_t launch_render(const RenderParams& p, int sigma_dtype, int uvw_dtype, bool stats,
                          hipStream_t stream)
 {
     const bool s16 = sigma_dtype == SQN_F16, u16 = uvw_dtype == SQN_F16;
+    if (p.linear)
+        return u16 ? launch_linear_d<_Float16>(p, stats, stream) : launch_linear_d<float>(p, stats, stream);
     if (s16 && u16)
         return launch_d<_Float16, _Float16>(p, stats, stream);
     if (s16)

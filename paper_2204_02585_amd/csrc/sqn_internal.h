@@ -42,6 +42,11 @@ struct RenderParams {
     float leap_margin;        // texels a leap keeps from its square's edge
     int32_t tiles_x, tiles_y; // workgroup tiles per view
     int32_t n_groups;         // workgroups in the grid
+    // linear (Eq. 5) decoder; sigma[j] then holds per-plane partial sums
+    int32_t linear;           // 1: Eq. 5, 0: Eq. 4
+    float b_sigma;            // density bias
+    const float* lin_w;       // [9D + 3][D]: rows c*3D + e of W_c^T, then b_u, b_v, b_w
+    int32_t lin_stride;       // LDS floats per ray of the folded weights
 };
 
 // Launch one render over all views on `stream`; `stats` selects the variant
@@ -53,11 +58,40 @@ hipError_t launch_render(const RenderParams& p, int sigma_dtype, int uvw_dtype,
 // Cap of the stored Chebyshev distance to the nearest occupied texel.
 constexpr int32_t kDistCap = 255;
 
+// Temporary device buffers of the create-time preparation.
+struct PrepareWork {
+    uint8_t* live;        // [n_p^2] 1 where a texel may give sigma > 0
+    uint16_t* f;          // [n_p^2] row distances
+    uint16_t* dist;       // [n_p^2] capped Chebyshev distances
+    float* maxima;        // [6][n_p] row / column maxima of the partial sums
+    float* w_sigma;       // [3 d_sigma] density weights (linear decoder)
+};
+
 // Pack sigma plane j (n_p x n_p of sigma_dtype, device memory) into
 // `packed` (4-byte records for binary16 sigma, 8-byte for binary32) with the
-// capped distance transform; work_f and work_dist are n_p^2 scratch words.
+// capped distance transform.
 hipError_t prepare_sigma_plane(const void* sigma, int sigma_dtype, int32_t n_p, void* packed,
-                               uint16_t* work_f, uint16_t* work_dist, hipStream_t stream);
+                               const PrepareWork& work, hipStream_t stream);
+
+// Linear (Eq. 5) decoder: fold each plane's sigma^j vectors
+// ([n_p][n_p][d_sigma] of sigma_dtype) with its block of W_sigma into
+// per-texel partial sums, mark the texels whose samples are empty whatever
+// the other two planes hold, and write 8-byte records (partial sum, capped
+// distance to the nearest texel not so marked) to packed[j].
+hipError_t prepare_linear_planes(const void* const sigma[3], int sigma_dtype, int32_t n_p,
+                                 int32_t d_sigma, float b_sigma, void* const packed[3],
+                                 const PrepareWork& work, hipStream_t stream);
+
+// Per-ray LDS floats of the folded Eq. 5 radiance weights: n values padded
+// to 4 (mod 8) words so that 16 rays' 16-byte reads spread over the banks.
+constexpr int32_t lin_pad(int32_t n)
+{
+    const int32_t m = (n + 3) / 4 * 4;
+    return m % 8 == 0 ? m + 4 : m;
+}
+// 9D + 3 rows for a compile-time D; 10D + 3 (rows, then beta) otherwise.
+constexpr int32_t lin_stride(int32_t D) { return lin_pad(9 * D + 3); }
+constexpr int32_t lin_stride_generic(int32_t D) { return lin_pad(10 * D + 3); }
 
 // Workgroup geometry: 256 threads = 4 wave64; with L lanes per ray a wave
 // holds 64/L rays laid out as a wave tile of kWaveW(L) x kWaveH(L) pixels and

@@ -23,6 +23,8 @@ def gpu_render(scene, t_eps=None, poses=None, n_samples=None, stats=True, mode="
     from paper_2204_02585_amd import binding
     caches = binding.caches_from_scene(scene, t_eps=t_eps)
     lanes, skip = MODES[mode]
+    print(f"[render {scene.config.name} {scene.config.width}x{scene.config.height}"
+          f"x{scene.config.n_poses} mode={mode}]", flush=True)
     caches.set_lanes_per_ray(lanes)
     caches.set_empty_space_skipping(skip)
     P = torch.from_numpy(scene.poses if poses is None else poses).cuda()

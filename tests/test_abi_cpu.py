@@ -78,3 +78,42 @@ def test_validation_before_device_calls(lib):
                               None) == lib.SQN_ERR_INVALID_ARG
     assert lib.lib.sqn_cache_device_bytes(None) == 0
     lib.lib.sqn_destroy(None)
+
+
+def test_linear_decoder_validation_before_device_calls(lib):
+    """sqn_create_linear_caches rejects a NULL decoder, d_sigma outside
+    [1, 64], NULL weight arrays and non-finite weights before touching the
+    device."""
+    import numpy as np
+    vp = ctypes.c_void_p
+    out = vp()
+    planes = (vp * 3)()
+    desc = lib.CacheDesc()
+    desc.n_p, desc.D, desc.n_theta, desc.n_phi = 64, 2, 4, 4
+    for r in range(3):
+        desc.bbox_min[r], desc.bbox_max[r] = -1.0, 1.0
+    desc.t_eps = 1e-4
+    ws = np.ones(3 * 4, np.float32)
+    wu = np.ones((3, 2, 6), np.float32)
+    bu = np.zeros((3, 2), np.float32)
+
+    def create(dec):
+        return lib.lib.sqn_create_linear_caches(ctypes.byref(desc), dec, planes, planes, None,
+                                                None, ctypes.byref(out))
+
+    def dec(ds=4, b=0.0, w_s=ws, w_u=wu, b_u=bu):
+        return ctypes.byref(lib.LinearDecoder(ds, b, w_s.ctypes.data if w_s is not None else None,
+                                              w_u.ctypes.data if w_u is not None else None,
+                                              b_u.ctypes.data if b_u is not None else None))
+
+    assert create(None) == lib.SQN_ERR_INVALID_ARG and "decoder" in lib.last_error()
+    assert create(dec(ds=0)) == lib.SQN_ERR_INVALID_ARG and "d_sigma" in lib.last_error()
+    assert create(dec(ds=65)) == lib.SQN_ERR_INVALID_ARG
+    assert create(dec(w_s=None)) == lib.SQN_ERR_INVALID_ARG
+    assert create(dec(b=float("inf"))) == lib.SQN_ERR_INVALID_ARG
+    wu[2, 1, 5] = np.nan
+    assert create(dec()) == lib.SQN_ERR_INVALID_ARG and "w_uvw[35]" in lib.last_error()
+    wu[2, 1, 5] = 1.0
+    # a valid decoder reaches the plane checks
+    assert create(dec()) == lib.SQN_ERR_INVALID_ARG and "sigma_planes" in lib.last_error()
+    assert not out
