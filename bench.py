@@ -32,6 +32,8 @@ WORKLOAD_TEXT = {
     "large": "800x800 image, 192 uniform samples/ray, k=1024 D=8 fp16 caches, 384x384 fp16 direction cache, 64 blobs sigma_max 200",
     "batch": "100 spiral views of 800x800, 192 uniform samples/ray, k=256 D=8 fp16 caches, 128x128 fp16 direction cache",
     "stress": "1920x1080 image, 384 stratified samples/ray, k=2048 D=16 fp16 caches, 512x512 fp16 direction cache, 256 blobs",
+    "alt": "Eq. 5 linear decoder (D_sigma=12): 800x800 image, 192 uniform samples/ray, k=256 D=8 fp16 caches, 128x128 fp16 direction cache, 64 blobs",
+    "alt512": "Eq. 5 linear decoder (D_sigma=12) at the paper's alt cache size: 800x800 image, 192 uniform samples/ray, k=512 D=8 fp16 caches, 256x256 fp16 direction cache, 64 blobs",
 }
 
 
@@ -39,10 +41,14 @@ def algorithmic_bytes(cfg, n_rays, live_inbox, occupied):
     """Bytes the method must move per launch: per ray the 4 direction-cache
     texels (D values each), the pose row reads are broadcast and not
     counted, 16 B of output (rgb + depth); per live in-box sample the three
-    sigma^j; per live occupied sample the three uvw records (3D values)."""
+    sigma^j (for the Eq. 5 decoder the three binary32 per-plane partial
+    sums the caches are folded into; its radiance weights are read once per
+    ray from cache and not counted); per live occupied sample the three uvw
+    records (3D values)."""
     b = 2 if cfg.dtype == "f16" else 4
+    b_sigma = 4 if cfg.sigma_channels > 0 else b
     per_ray = 4 * cfg.D * b + 16
-    return n_rays * per_ray + live_inbox * 3 * b + occupied * 3 * 3 * cfg.D * b
+    return n_rays * per_ray + live_inbox * 3 * b_sigma + occupied * 3 * 3 * cfg.D * b
 
 
 def measured_traffic(config_name):
@@ -186,6 +192,8 @@ def main():
                    "views_per_step": B, "width": cfg.width, "height": cfg.height,
                    "samples_per_ray": N, "n_p": cfg.n_p, "D": cfg.D, "cache_dtype": cfg.dtype,
                    "direction_cache": [cfg.n_theta, cfg.n_phi], "t_eps": cfg.t_eps,
+                   "decoder": ("Eq. 5 linear, D_sigma=%d" % cfg.sigma_channels
+                               if cfg.sigma_channels > 0 else "Eq. 4 product/sum"),
                    "lanes_per_ray": args.lanes or "auto",
                    "empty_space_leaps": not args.dense},
         "frames_per_s": round(fps, 2),
@@ -193,7 +201,8 @@ def main():
                     "occupied_per_step": occupied},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic(cfg.name) if args.lanes == 0 else None,
+                     "traffic": (measured_traffic(cfg.name)
+                                 if args.lanes == 0 and not args.dense else None),
                      "algorithmic_bytes_per_launch": int(bytes_alg),
                      "kernel_ms_per_launch": round(ms, 5)},
         "cpu_baseline": base,

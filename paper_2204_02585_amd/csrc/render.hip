@@ -846,13 +846,16 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
     }
     if (s != 0)
         return;
+    // outputs are written once and never read here: streaming stores keep
+    // the partially written lines of a pixel tile from being allocated in
+    // L2 and written back piecemeal while the gathers churn it
     if (P.rgb) {
-        P.rgb[3 * ray + 0] = static_cast<float>(acc_r);
-        P.rgb[3 * ray + 1] = static_cast<float>(acc_g);
-        P.rgb[3 * ray + 2] = static_cast<float>(acc_b);
+        __builtin_nontemporal_store(static_cast<float>(acc_r), P.rgb + 3 * ray + 0);
+        __builtin_nontemporal_store(static_cast<float>(acc_g), P.rgb + 3 * ray + 1);
+        __builtin_nontemporal_store(static_cast<float>(acc_b), P.rgb + 3 * ray + 2);
     }
     if (P.depth)
-        P.depth[ray] = static_cast<float>(acc_t);
+        __builtin_nontemporal_store(static_cast<float>(acc_t), P.depth + ray);
     if constexpr (STATS) {
         uint4 st;
         st.x = static_cast<uint32_t>(stop);
