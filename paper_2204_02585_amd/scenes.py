@@ -326,3 +326,81 @@ def make_scene(name_or_config, n_poses: Optional[int] = None) -> Scene:
     beta = uniform_pm1((cfg.n_theta, cfg.n_phi, cfg.D), dt, rng_beta)
     poses = single_pose() if cfg.n_poses == 1 else spiral_poses(cfg.n_poses)
     return Scene(cfg, sigma, uvw, beta, poses, seed=4000 + n, decoder=decoder)
+
+
+# --------------------------------------------------------------------------
+# cache generation: synthetic network weights (no trained weights exist here)
+
+@dataclasses.dataclass(frozen=True)
+class GenConfig:
+    """One cache-generation workload: grid sizes and network shapes
+    (Sec. 3.4: position networks of 6 layers x 256 units, direction network
+    of 4 layers x 128 units; NeRF encodings with 10 and 4 frequencies)."""
+    name: str
+    number: int
+    n_p: int
+    n_theta: int
+    n_phi: int
+    D: int = 8
+    pos_layers: int = 6
+    pos_width: int = 256
+    dir_layers: int = 4
+    dir_width: int = 128
+    pos_freq: int = 10
+    dir_freq: int = 4
+
+    @property
+    def pos_in(self) -> int:
+        return 2 * (1 + 2 * self.pos_freq)
+
+    @property
+    def dir_in(self) -> int:
+        return 3 * (1 + 2 * self.dir_freq)
+
+    @property
+    def pos_out(self) -> int:
+        return 2 + 6 * self.D
+
+
+GEN_CONFIGS = {
+    "gen_tiny": GenConfig("gen_tiny", 11, 32, 16, 16),
+    # the paper's 512 cache (n_d = 64 on the synthetic scenes, Sec. 3.3)
+    "gen_512": GenConfig("gen_512", 12, 512, 64, 64),
+    # the 1K cache whose generation Table 4 times
+    "gen_1k": GenConfig("gen_1k", 13, 1024, 64, 64),
+}
+
+
+def mlp_weights(sizes, seed: int, out_scale: float = 1.0):
+    """[(W [out][in] binary16, b [out] binary32), ...] for the layer sizes
+    sizes[0] -> sizes[1] -> ... : hidden layers He-uniform
+    (+-sqrt(6 / fan_in)), the last layer uniform in +-out_scale/sqrt(fan_in);
+    biases uniform in +-0.1."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    layers = []
+    for n, (fi, fo) in enumerate(zip(sizes[:-1], sizes[1:])):
+        last = n == len(sizes) - 2
+        lim = out_scale / math.sqrt(fi) if last else math.sqrt(6.0 / fi)
+        W = rng.uniform(-lim, lim, size=(fo, fi)).astype(np.float16)
+        b = rng.uniform(-0.1, 0.1, size=fo).astype(np.float32)
+        layers.append((W, b))
+    return layers
+
+
+@dataclasses.dataclass
+class GenScene:
+    config: GenConfig
+    pos: list          # three layer lists, planes xy, yz, zx
+    dir: list
+    bbox_min: tuple = BOX_MIN
+    bbox_max: tuple = BOX_MAX
+
+
+def make_gen_scene(name_or_config) -> GenScene:
+    cfg = GEN_CONFIGS[name_or_config] if isinstance(name_or_config, str) else name_or_config
+    n = cfg.number
+    pos_sizes = [cfg.pos_in] + [cfg.pos_width] * cfg.pos_layers + [cfg.pos_out]
+    dir_sizes = [cfg.dir_in] + [cfg.dir_width] * cfg.dir_layers + [cfg.D]
+    pos = [mlp_weights(pos_sizes, 7000 + 10 * n + j, out_scale=1.5) for j in range(3)]
+    dirw = mlp_weights(dir_sizes, 7000 + 10 * n + 5, out_scale=1.5)
+    return GenScene(cfg, pos, dirw)
