@@ -89,12 +89,115 @@ def cpu_baseline(scene, budget_s=12.0, max_frames=40):
                       f"{el:.1f} s wall", "frames_per_s": frames / el}
 
 
+GEN_TEXT = {
+    "gen_tiny": "cache generation: 3 position networks (6x256) on 32x32 grids, direction network (4x128) on 16x16 nodes, D=8",
+    "gen_512": "cache generation for the paper's 512 cache: 3 position networks (6x256, NeRF encoding L=10) on 512x512 grids, direction network (4x128, L=4) on 64x64 nodes, D=8",
+    "gen_1k": "cache generation for the paper's 1K cache (Table 4): 3 position networks (6x256, NeRF encoding L=10) on 1024x1024 grids, direction network (4x128, L=4) on 64x64 nodes, D=8",
+}
+MFMA_F16_PEAK_TFLOPS = 2500.0
+
+
+def network_flops(cfg):
+    """Multiply-adds x 2 of the networks as specified (unpadded): per
+    position point n_in W + (L - 1) W^2 + W n_out, per direction node the
+    same with the direction shapes."""
+    pos = cfg.pos_in * cfg.pos_width + (cfg.pos_layers - 1) * cfg.pos_width ** 2 + cfg.pos_width * cfg.pos_out
+    dirn = cfg.dir_in * cfg.dir_width + (cfg.dir_layers - 1) * cfg.dir_width ** 2 + cfg.dir_width * cfg.D
+    return 2 * pos, 2 * dirn
+
+
+def bench_generate(args):
+    """One step = one sqn_generate_caches call: all three position grids and
+    the direction grid, written into resident output buffers."""
+    import torch
+    from paper_2204_02585_amd import binding, scenes
+    g = scenes.make_gen_scene(args.config)
+    cfg = g.config
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    nets = binding.networks_from_gen_scene(g)
+    n_pos = 3 * cfg.n_p * cfg.n_p
+    n_dir = cfg.n_theta * cfg.n_phi
+    out = ([torch.empty((cfg.n_p, cfg.n_p), dtype=torch.float32, device=dev) for _ in range(3)],
+           [torch.empty((cfg.n_p, cfg.n_p, 3 * cfg.D), dtype=torch.float16, device=dev) for _ in range(3)],
+           torch.empty((cfg.n_theta, cfg.n_phi, cfg.D), dtype=torch.float16, device=dev))
+    stream = torch.cuda.current_stream()
+
+    def step():
+        nets.generate(cfg.n_p, cfg.n_theta, cfg.n_phi, g.bbox_min, g.bbox_max, out=out, stream=stream)
+
+    print(f"[bench] {cfg.name}: warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = ev0.elapsed_time(ev1) / args.steps
+    f_pos, f_dir = network_flops(cfg)
+    flops = n_pos * f_pos + n_dir * f_dir
+    tflops = flops / (ms * 1e-3) / 1e12
+
+    base = None
+    if not args.no_cpu_baseline:
+        # the binary64 oracle on a bounded sample of position points
+        print("[bench] CPU oracle baseline", file=sys.stderr, flush=True)
+        import numpy as np
+        from oracle import cachegen
+        rng = np.random.Generator(np.random.PCG64(1))
+        n_s = 0
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < args.cpu_budget and n_s < 3 * 65536:
+            ia = rng.integers(0, cfg.n_p, 8192)
+            ib = rng.integers(0, cfg.n_p, 8192)
+            cachegen.position_cache_points(g.pos[n_s % 3], cfg.n_p, n_s % 3, g.bbox_min, g.bbox_max, cfg.D,
+                                           ia, ib, cfg.pos_freq)
+            n_s += 8192
+        el = time.perf_counter() - t0
+        threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or (os.cpu_count() or 1)
+        base = {"value": round(n_s / el / 1e6, 4), "unit": "Mpoints/s", "cores": threads, "kind": "oracle",
+                "sample": f"{n_s} random position-grid points (binary64 numpy, BLAS threads as configured), "
+                          f"{el:.1f} s wall"}
+    nets.close()
+    out_line = {
+        "metric": "cache generation: Mpoints/s of network evaluations on the cache grids",
+        "value": round((n_pos + n_dir) / (ms * 1e-3) / 1e6, 2),
+        "unit": "Mpoints/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic (seeded He-uniform binary16 weights; no trained networks)",
+        "config": {"workload": f"{cfg.name}: {GEN_TEXT[cfg.name]}", "n_p": cfg.n_p,
+                   "direction_grid": [cfg.n_theta, cfg.n_phi], "D": cfg.D,
+                   "position_points": n_pos, "direction_points": n_dir},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_F16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(tflops / MFMA_F16_PEAK_TFLOPS, 4), "traffic": None,
+                     "algorithmic_flops_per_launch": int(flops), "kernel_ms_per_launch": round(ms, 4)},
+        "cpu_baseline": base,
+        "wall_s_timed": round(wall, 4),
+    }
+    print(json.dumps(out_line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", default="paper", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--config", default="paper", choices=sorted(WORKLOAD_TEXT) + sorted(GEN_TEXT),
+                    help="a render workload, or gen_* for cache generation")
     ap.add_argument("--lanes", type=int, default=0,
                     help="lanes of a wavefront per ray (1, 2, 4); 0 = the library's choice")
     ap.add_argument("--dense", action="store_true",
@@ -110,6 +213,10 @@ def main():
         print("bench.py measures one GPU: the render path has no cross-GPU step; "
               "run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
+
+    if args.config in GEN_TEXT:
+        bench_generate(args)
+        return
 
     import torch
     from paper_2204_02585_amd import binding, scenes

@@ -214,6 +214,69 @@ sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes);
  * Errors: SQN_ERR_INVALID_ARG. */
 sqn_status sqn_set_empty_space_skipping(sqn_caches* caches, int32_t enable);
 
+/* ---- cache generation (Sec. 3.3; network shapes of Sec. 3.4) --------------
+ *
+ * The caches are the outputs of the trained networks on grids: each position
+ * network F_pos^j on its plane's n_p x n_p vertex-aligned nodes over the
+ * scene box (plane j = (first, second) axes of xy, yz, zx, indexed
+ * [first][second]), the direction network F_dir on the n_theta x n_phi
+ * direction nodes (theta_a = a pi / (n_theta - 1) from +z, phi_b =
+ * -pi + b 2 pi / n_phi).  Inputs are NeRF's positional encoding, per
+ * component c of the input: [c, then for k = 0..L-1: sin(2^k pi c),
+ * cos(2^k pi c)], interleaved over the components per frequency, i.e.
+ * [a, b, sin(pi a), sin(pi b), cos(pi a), cos(pi b), sin(2 pi a), ...].
+ * Hidden layers apply ReLU, the last layer is linear.  F_pos^j emits
+ * (sigma_0, w_sigma, w_u[D], u_0[D], w_v[D], v_0[D], w_w[D], w_0[D]) (the
+ * order of Sec. 3.2) and the cache stores Eq. 3's sigma^j = sigma_0 w_sigma
+ * and k^j = w_k * k_0; F_dir emits beta[D].
+ * Arithmetic: binary16 weights and activations, binary32 accumulation,
+ * biases, Eq. 3 products and outputs before their storage dtype. */
+
+/* One network, host memory read during sqn_create_networks only. */
+typedef struct {
+    int32_t n_hidden;                 /* hidden layers, 1..16                         */
+    int32_t width;                    /* units per hidden layer: 256 for F_pos^j, 128  */
+                                      /* for F_dir (the sizes of Sec. 3.4)            */
+    int32_t n_in;                     /* encoding size: 2 (1 + 2 pos_freq) or          */
+                                      /* 3 (1 + 2 dir_freq), at most 64               */
+    int32_t n_out;                    /* 2 + 6D for F_pos^j, D for F_dir               */
+    const uint16_t* const* weights;   /* n_hidden + 1 binary16 matrices [out][in]      */
+    const float* const* biases;       /* n_hidden + 1 binary32 vectors [out]           */
+} sqn_mlp_desc;
+
+/* Opaque, library-owned device copy of the four networks. */
+typedef struct sqn_networks sqn_networks;
+
+/* Upload the networks (pos[j] for planes xy, yz, zx, and dir) for outputs of
+ * D components, with pos_freq / dir_freq encoding frequencies (NeRF: 10, 4).
+ * Weights must be finite.  The call waits for its copies; *out is NULL on
+ * failure.  Errors: SQN_ERR_INVALID_ARG (NULL, sizes, non-finite values),
+ * SQN_ERR_UNSUPPORTED (other widths), SQN_ERR_OUT_OF_MEMORY,
+ * SQN_ERR_DEVICE. */
+sqn_status sqn_create_networks(const sqn_mlp_desc pos[3], const sqn_mlp_desc* dir,
+                               int32_t D, int32_t pos_freq, int32_t dir_freq,
+                               void* stream, sqn_networks** out);
+
+/* Evaluate the networks on the grids desc describes (n_p, n_theta, n_phi,
+ * D, bbox and the three dtypes; the sampling fields are ignored) and write
+ * the caches in the layout sqn_create_caches reads:
+ *   sigma_planes[j]: device, [n_p][n_p] of sigma_dtype;
+ *   uvw_planes[j]:   device, [n_p][n_p][3D] of uvw_dtype;
+ *   beta:            device, [n_theta][n_phi][D] of beta_dtype.
+ * Asynchronous on `stream`; allocates nothing.  The handle keeps one
+ * encoding table, so generations with one handle must not overlap.
+ * Errors: SQN_ERR_INVALID_ARG (desc, D mismatch, output buffers that are
+ * not device allocations large enough, wrong device), SQN_ERR_DEVICE. */
+sqn_status sqn_generate_caches(sqn_networks* nets, const sqn_cache_desc* desc,
+                               void* const sigma_planes[3], void* const uvw_planes[3],
+                               void* beta, void* stream);
+
+/* Bytes of device memory the networks handle owns. */
+size_t sqn_networks_device_bytes(const sqn_networks* nets);
+
+/* Free the networks; NULL is a no-op. */
+void sqn_destroy_networks(sqn_networks* nets);
+
 /* Bytes of device memory the handle owns. */
 size_t sqn_cache_device_bytes(const sqn_caches* caches);
 

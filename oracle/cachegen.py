@@ -109,3 +109,17 @@ def caches(pos_layers: List, dir_layers, n_p: int, n_theta: int, n_phi: int, bmi
         sig.append(s)
         uvw.append(u)
     return sig, uvw, direction_cache(dir_layers, n_theta, n_phi, dir_freq)
+
+
+def position_cache_points(layers, n_p: int, plane: int, bmin, bmax, D: int, ia, ib,
+                          n_freq: int = 10) -> Tuple[np.ndarray, np.ndarray]:
+    """position_cache at the grid points (ia[n], ib[n]) only: (sigma^j [n],
+    uvw^j [n][3D])."""
+    ra, rb = PLANE_AXES[plane]
+    a = grid_nodes(n_p, bmin[ra], bmax[ra])[np.asarray(ia)]
+    b = grid_nodes(n_p, bmin[rb], bmax[rb])[np.asarray(ib)]
+    o = mlp(encode(np.stack([a, b], axis=-1), n_freq), layers)
+    sigma = o[..., 0] * o[..., 1]
+    uvw = [o[..., 2 + 2 * c * D: 2 + (2 * c + 1) * D] * o[..., 2 + (2 * c + 1) * D: 2 + (2 * c + 2) * D]
+           for c in range(3)]
+    return sigma, np.concatenate(uvw, axis=-1)

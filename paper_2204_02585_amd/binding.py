@@ -20,7 +20,8 @@ SQN_F32, SQN_F16 = 0, 1
 
 EXPORTS = ("sqn_create_caches", "sqn_create_linear_caches", "sqn_render", "sqn_render_stats",
            "sqn_set_lanes_per_ray", "sqn_set_empty_space_skipping", "sqn_cache_device_bytes",
-           "sqn_destroy", "sqn_status_string", "sqn_last_error")
+           "sqn_destroy", "sqn_status_string", "sqn_last_error", "sqn_create_networks",
+           "sqn_generate_caches", "sqn_networks_device_bytes", "sqn_destroy_networks")
 
 
 class CacheDesc(ctypes.Structure):
@@ -37,6 +38,13 @@ class LinearDecoder(ctypes.Structure):
     _fields_ = [("d_sigma", ctypes.c_int32), ("b_sigma", ctypes.c_float),
                 ("w_sigma", ctypes.c_void_p), ("w_uvw", ctypes.c_void_p),
                 ("b_uvw", ctypes.c_void_p)]
+
+
+class MLPDesc(ctypes.Structure):
+    _fields_ = [("n_hidden", ctypes.c_int32), ("width", ctypes.c_int32),
+                ("n_in", ctypes.c_int32), ("n_out", ctypes.c_int32),
+                ("weights", ctypes.POINTER(ctypes.c_void_p)),
+                ("biases", ctypes.POINTER(ctypes.c_void_p))]
 
 
 class Intrinsics(ctypes.Structure):
@@ -65,6 +73,16 @@ def _load() -> ctypes.CDLL:
     lib.sqn_create_linear_caches.argtypes = [ctypes.POINTER(CacheDesc), ctypes.POINTER(LinearDecoder),
                                              ctypes.POINTER(vp), ctypes.POINTER(vp), vp, vp,
                                              ctypes.POINTER(vp)]
+    lib.sqn_create_networks.restype = ctypes.c_int
+    lib.sqn_create_networks.argtypes = [ctypes.POINTER(MLPDesc), ctypes.POINTER(MLPDesc), i32, i32, i32,
+                                        vp, ctypes.POINTER(vp)]
+    lib.sqn_generate_caches.restype = ctypes.c_int
+    lib.sqn_generate_caches.argtypes = [vp, ctypes.POINTER(CacheDesc), ctypes.POINTER(vp),
+                                        ctypes.POINTER(vp), vp, vp]
+    lib.sqn_networks_device_bytes.restype = ctypes.c_size_t
+    lib.sqn_networks_device_bytes.argtypes = [vp]
+    lib.sqn_destroy_networks.restype = None
+    lib.sqn_destroy_networks.argtypes = [vp]
     lib.sqn_render.restype = ctypes.c_int
     lib.sqn_render.argtypes = [vp, vp, i32, ctypes.POINTER(Intrinsics), f32, f32, i32, vp, vp, vp]
     lib.sqn_render_stats.restype = ctypes.c_int
@@ -247,3 +265,93 @@ def caches_from_scene(scene, device="cuda", t_eps=None, stratified=None, stream=
                     stratified=cfg.stratified if stratified is None else stratified,
                     seed=scene.seed, stream=stream, decoder=getattr(scene, "decoder", None))
     return caches
+
+
+# ---------------------------------------------------------------- cache generation
+
+class _MLP:
+    """Keeps the host arrays of one network alive while its descriptor is in
+    use; the descriptor states the shapes the arrays really have."""
+
+    def __init__(self, layers):
+        import numpy as np
+        self.W = [np.ascontiguousarray(W, dtype=np.float16) for W, _ in layers]
+        self.b = [np.ascontiguousarray(b, dtype=np.float32) for _, b in layers]
+        width = self.W[0].shape[0]
+        for n, (W, b) in enumerate(zip(self.W, self.b)):
+            fi = self.W[0].shape[1] if n == 0 else width
+            fo = self.W[-1].shape[0] if n == len(self.W) - 1 else width
+            if W.shape != (fo, fi) or b.shape != (fo,):
+                raise ValueError(f"layer {n}: weight {W.shape} / bias {b.shape} do not chain")
+        self.wp = (ctypes.c_void_p * len(self.W))(*[w.ctypes.data for w in self.W])
+        self.bp = (ctypes.c_void_p * len(self.b))(*[b.ctypes.data for b in self.b])
+        self.desc = MLPDesc(len(layers) - 1, width, self.W[0].shape[1], self.W[-1].shape[0],
+                            ctypes.cast(self.wp, ctypes.POINTER(ctypes.c_void_p)),
+                            ctypes.cast(self.bp, ctypes.POINTER(ctypes.c_void_p)))
+
+
+class Networks:
+    """Library-owned device copy of the position and direction networks
+    (sqn_create_networks); layers are lists of (W [out][in] binary16,
+    b [out] binary32)."""
+
+    def __init__(self, pos_layers, dir_layers, D: int, pos_freq: int = 10, dir_freq: int = 4,
+                 stream=None):
+        self._h = ctypes.c_void_p(None)
+        pos = [_MLP(l) for l in pos_layers]
+        dirn = _MLP(dir_layers)
+        arr = (MLPDesc * 3)(*[m.desc for m in pos])
+        _check(lib.sqn_create_networks(arr, ctypes.byref(dirn.desc), int(D), int(pos_freq), int(dir_freq),
+                                       _stream(stream), ctypes.byref(self._h)))
+        self.D = D
+
+    @property
+    def handle(self) -> ctypes.c_void_p:
+        if not self._h:
+            raise ValueError("networks have been destroyed")
+        return self._h
+
+    @property
+    def device_bytes(self) -> int:
+        return int(lib.sqn_networks_device_bytes(self.handle))
+
+    def generate(self, n_p: int, n_theta: int, n_phi: int, bbox_min, bbox_max,
+                 sigma_dtype=torch.float32, uvw_dtype=torch.float16, beta_dtype=torch.float16,
+                 out=None, stream=None, device="cuda"):
+        """sqn_generate_caches; returns ([sigma^j], [uvw^j], beta) device tensors
+        (or fills `out`, a tuple of that form)."""
+        D = self.D
+        if out is None:
+            sig = [torch.empty((n_p, n_p), dtype=sigma_dtype, device=device) for _ in range(3)]
+            uvw = [torch.empty((n_p, n_p, 3 * D), dtype=uvw_dtype, device=device) for _ in range(3)]
+            beta = torch.empty((n_theta, n_phi, D), dtype=beta_dtype, device=device)
+        else:
+            sig, uvw, beta = out
+        desc = CacheDesc()
+        desc.n_p, desc.D, desc.n_theta, desc.n_phi = n_p, D, n_theta, n_phi
+        desc.sigma_dtype, desc.uvw_dtype, desc.beta_dtype = (_dtype_code(sig[0]), _dtype_code(uvw[0]),
+                                                             _dtype_code(beta))
+        for r in range(3):
+            desc.bbox_min[r] = bbox_min[r]
+            desc.bbox_max[r] = bbox_max[r]
+        desc.t_eps = 0.0
+        sp = (ctypes.c_void_p * 3)(*[t.data_ptr() for t in sig])
+        up = (ctypes.c_void_p * 3)(*[t.data_ptr() for t in uvw])
+        _check(lib.sqn_generate_caches(self.handle, ctypes.byref(desc), sp, up, _ptr(beta), _stream(stream)))
+        return sig, uvw, beta
+
+    def close(self) -> None:
+        if self._h:
+            lib.sqn_destroy_networks(self._h)
+            self._h = ctypes.c_void_p(None)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def networks_from_gen_scene(gscene, stream=None) -> Networks:
+    c = gscene.config
+    return Networks(gscene.pos, gscene.dir, c.D, c.pos_freq, c.dir_freq, stream=stream)

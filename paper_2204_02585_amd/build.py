@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB_PATH = os.path.join(PKG, "libsqn.so")
 SOURCES = [os.path.join(CSRC, "api.hip"), os.path.join(CSRC, "render.hip"),
-           os.path.join(CSRC, "prepare.hip")]
+           os.path.join(CSRC, "prepare.hip"), os.path.join(CSRC, "generate.hip")]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

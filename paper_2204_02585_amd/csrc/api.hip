@@ -32,6 +32,17 @@ struct sqn_caches {
     const float* lin_w;      // [9D + 3][D] folded radiance weights and biases
 };
 
+// Device copy of the networks for cache generation.
+struct sqn_networks {
+    int device;
+    void* block;             // one hipMalloc: fragments, biases, encoding table
+    size_t bytes;
+    sqn::GenNet pos[3];
+    sqn::GenNet dir;
+    int32_t D, pos_freq, dir_freq, pos_in, dir_in;
+    _Float16* enc_table;     // 3 x 8192 x (1 + 2 pos_freq) binary16
+};
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -453,6 +464,96 @@ sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec
     return SQN_OK;
 }
 
+// ---- cache generation: networks on the host side ---------------------------
+
+// the input unit held by element e of lane-half h in a K step (generate.hip)
+int kmap(int h, int e) { return 8 * (e >> 2) + 4 * h + (e & 3); }
+
+bool half_finite(uint16_t bits) { return (bits & 0x7c00u) != 0x7c00u; }
+
+// W [n_out][n_in] (binary16 bits) as MFMA A fragments
+// [chunk][tile][step][lane][8] for `tiles` 32-row tiles and `steps` K steps
+// of 16 inputs (steps a multiple of 4); physical row r takes source row
+// rowmap[r] (-1: zero row), lane l covers row 32 tile + l % 32 and inputs
+// 16 step + kmap(l / 32, e).
+void build_fragments(const uint16_t* W, int n_in, const std::vector<int>& rowmap, int tiles, int steps,
+                     uint16_t* out)
+{
+    size_t o = 0;
+    for (int c = 0; c < steps / 4; ++c)
+        for (int m = 0; m < tiles; ++m)
+            for (int ss = 0; ss < 4; ++ss)
+                for (int lane = 0; lane < 64; ++lane)
+                    for (int e = 0; e < 8; ++e) {
+                        const int src = rowmap[32 * m + lane % 32];
+                        const int u = 16 * (4 * c + ss) + kmap(lane / 32, e);
+                        out[o++] = (src >= 0 && u < n_in) ? W[static_cast<size_t>(src) * n_in + u] : 0;
+                    }
+}
+
+sqn_status validate_mlp(const sqn_mlp_desc* m, int width, int n_in, int n_out, const char* what)
+{
+    if (!m)
+        return fail(SQN_ERR_INVALID_ARG, "%s is NULL", what);
+    if (m->width != width)
+        return fail(SQN_ERR_UNSUPPORTED, "%s: width %d (this build runs %d units)", what, m->width, width);
+    if (m->n_hidden < 1 || m->n_hidden > sqn::kMaxHidden)
+        return fail(SQN_ERR_INVALID_ARG, "%s: n_hidden = %d outside [1, %d]", what, m->n_hidden, sqn::kMaxHidden);
+    if (m->n_in != n_in || m->n_out != n_out)
+        return fail(SQN_ERR_INVALID_ARG, "%s: %d inputs / %d outputs, expected %d / %d", what, m->n_in,
+                    m->n_out, n_in, n_out);
+    if (!m->weights || !m->biases)
+        return fail(SQN_ERR_INVALID_ARG, "%s: NULL weight or bias array", what);
+    for (int l = 0; l <= m->n_hidden; ++l) {
+        const int fi = l == 0 ? n_in : width, fo = l == m->n_hidden ? n_out : width;
+        if (!m->weights[l] || !m->biases[l])
+            return fail(SQN_ERR_INVALID_ARG, "%s: layer %d has a NULL array", what, l);
+        for (int k = 0; k < fi * fo; ++k)
+            if (!half_finite(m->weights[l][k]))
+                return fail(SQN_ERR_INVALID_ARG, "%s: layer %d weight %d is not finite", what, l, k);
+        for (int k = 0; k < fo; ++k)
+            if (!isfinite(m->biases[l][k]))
+                return fail(SQN_ERR_INVALID_ARG, "%s: layer %d bias %d is not finite", what, l, k);
+    }
+    return SQN_OK;
+}
+
+// Host image of one network: fragments and biases per layer, and where each
+// lands in the device block.
+struct NetImage {
+    std::vector<uint16_t> frag[sqn::kMaxHidden + 1];
+    std::vector<float> bias[sqn::kMaxHidden + 1];
+    int n_hidden = 0;
+    int out_tiles = 0;
+};
+
+// head_rows: physical row -> source output row of the head
+NetImage make_image(const sqn_mlp_desc* m, int width, int in_steps, const std::vector<int>& head_rows,
+                    int out_tiles)
+{
+    NetImage img;
+    img.n_hidden = m->n_hidden;
+    img.out_tiles = out_tiles;
+    std::vector<int> ident(width);
+    for (int r = 0; r < width; ++r)
+        ident[r] = r;
+    const int tiles = width / 32;
+    for (int l = 0; l <= m->n_hidden; ++l) {
+        const bool head = l == m->n_hidden;
+        const int fi = l == 0 ? m->n_in : width;
+        const int t = head ? out_tiles : tiles;
+        const int steps = l == 0 ? in_steps : width / 16;
+        const std::vector<int>& rows = head ? head_rows : ident;
+        img.frag[l].resize(static_cast<size_t>(t) * steps * 512);
+        build_fragments(m->weights[l], fi, rows, t, steps, img.frag[l].data());
+        img.bias[l].assign(static_cast<size_t>(t) * 32, 0.0f);
+        for (int r = 0; r < t * 32; ++r)
+            if (rows[r] >= 0)
+                img.bias[l][r] = m->biases[l][rows[r]];
+    }
+    return img;
+}
+
 }  // namespace
 
 extern "C" {
@@ -474,6 +575,193 @@ sqn_status sqn_create_linear_caches(const sqn_cache_desc* desc, const sqn_linear
         return fail(SQN_ERR_INVALID_ARG, "decoder is NULL");
     }
     return create_impl(desc, decoder, sigma_planes, uvw_planes, beta, stream, out);
+}
+
+sqn_status sqn_create_networks(const sqn_mlp_desc pos[3], const sqn_mlp_desc* dir, int32_t D,
+                               int32_t pos_freq, int32_t dir_freq, void* stream, sqn_networks** out)
+{
+    if (!out)
+        return fail(SQN_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    if (!pos)
+        return fail(SQN_ERR_INVALID_ARG, "pos is NULL");
+    if (D < 1 || D > 32)
+        return fail(SQN_ERR_INVALID_ARG, "D = %d outside [1, 32]", D);
+    const int pos_in = 2 * (1 + 2 * pos_freq), dir_in = 3 * (1 + 2 * dir_freq);
+    if (pos_freq < 0 || pos_in > 64 || dir_freq < 0 || dir_in > 64)
+        return fail(SQN_ERR_INVALID_ARG, "encoding frequencies %d / %d give more than 64 inputs", pos_freq,
+                    dir_freq);
+    static const char* names[3] = {"pos[0] (xy)", "pos[1] (yz)", "pos[2] (zx)"};
+    sqn_status s;
+    for (int j = 0; j < 3; ++j)
+        if ((s = validate_mlp(&pos[j], 256, pos_in, 2 + 6 * D, names[j])) != SQN_OK)
+            return s;
+    if ((s = validate_mlp(dir, 128, dir_in, D, "dir")) != SQN_OK)
+        return s;
+
+    // position head: pair slot P = 16 m + 8 gg + 4 h + q in rows
+    // 32 m + 16 gg + 4 h + q (first factor) and + 8 (second); slot 0 is
+    // (sigma_0, w_sigma), slot 1 + c D + d is (w_c[d], c_0[d]) (Eq. 3)
+    const int slots = 1 + 3 * D;
+    const int pos_tiles = (slots + 15) / 16;
+    std::vector<int> pos_rows(pos_tiles * 32, -1);
+    for (int slot = 0; slot < slots; ++slot) {
+        const int m = slot / 16, gg = (slot / 8) % 2, h = (slot / 4) % 2, q = slot % 4;
+        const int row = 32 * m + 16 * gg + 4 * h + q;
+        int first = 0, second = 1;
+        if (slot > 0) {
+            const int c = (slot - 1) / D, d = (slot - 1) % D;
+            first = 2 + 2 * c * D + d;
+            second = 2 + (2 * c + 1) * D + d;
+        }
+        pos_rows[row] = first;
+        pos_rows[row + 8] = second;
+    }
+    std::vector<int> dir_rows(32, -1);
+    for (int r = 0; r < D; ++r)
+        dir_rows[r] = r;
+
+    NetImage img[4];
+    for (int j = 0; j < 3; ++j)
+        img[j] = make_image(&pos[j], 256, 4, pos_rows, pos_tiles);
+    img[3] = make_image(dir, 128, 4, dir_rows, 1);
+
+    auto align = [](size_t x) { return (x + 255) & ~size_t{255}; };
+    size_t total = 0;
+    size_t off_frag[4][sqn::kMaxHidden + 1], off_bias[4][sqn::kMaxHidden + 1];
+    for (int n = 0; n < 4; ++n)
+        for (int l = 0; l <= img[n].n_hidden; ++l) {
+            off_frag[n][l] = total;
+            total += align(img[n].frag[l].size() * sizeof(uint16_t));
+            off_bias[n][l] = total;
+            total += align(img[n].bias[l].size() * sizeof(float));
+        }
+    const size_t off_table = total;
+    total += align(3 * size_t{8192} * (1 + 2 * pos_freq) * sizeof(uint16_t));
+
+    sqn_networks* h = static_cast<sqn_networks*>(calloc(1, sizeof(sqn_networks)));
+    if (!h)
+        return fail(SQN_ERR_OUT_OF_MEMORY, "host allocation failed");
+    if (hipGetDevice(&h->device) != hipSuccess) {
+        free(h);
+        return fail(SQN_ERR_DEVICE, "hipGetDevice failed");
+    }
+    hipError_t e = hipMalloc(&h->block, total);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        free(h);
+        return fail(SQN_ERR_OUT_OF_MEMORY, "hipMalloc(%zu) failed: %s", total, hipGetErrorString(e));
+    }
+    h->bytes = total;
+    char* base = static_cast<char*>(h->block);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    for (int n = 0; n < 4 && e == hipSuccess; ++n) {
+        sqn::GenNet& g = n < 3 ? h->pos[n] : h->dir;
+        g.n_hidden = img[n].n_hidden;
+        g.out_tiles = img[n].out_tiles;
+        for (int l = 0; l <= img[n].n_hidden && e == hipSuccess; ++l) {
+            g.frag[l] = base + off_frag[n][l];
+            g.bias[l] = reinterpret_cast<const float*>(base + off_bias[n][l]);
+            e = hipMemcpyAsync(base + off_frag[n][l], img[n].frag[l].data(),
+                               img[n].frag[l].size() * sizeof(uint16_t), hipMemcpyHostToDevice, st);
+            if (e == hipSuccess)
+                e = hipMemcpyAsync(base + off_bias[n][l], img[n].bias[l].data(),
+                                   img[n].bias[l].size() * sizeof(float), hipMemcpyHostToDevice, st);
+        }
+    }
+    if (e == hipSuccess)
+        e = hipStreamSynchronize(st);
+    else
+        (void)hipStreamSynchronize(st);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        (void)hipFree(h->block);
+        free(h);
+        return fail(SQN_ERR_DEVICE, "network upload failed: %s", hipGetErrorString(e));
+    }
+    h->enc_table = reinterpret_cast<_Float16*>(base + off_table);
+    h->D = D;
+    h->pos_freq = pos_freq;
+    h->dir_freq = dir_freq;
+    h->pos_in = pos_in;
+    h->dir_in = dir_in;
+    *out = h;
+    g_last_error.clear();
+    return SQN_OK;
+}
+
+sqn_status sqn_generate_caches(sqn_networks* nets, const sqn_cache_desc* desc, void* const sigma_planes[3],
+                               void* const uvw_planes[3], void* beta, void* stream)
+{
+    if (!nets)
+        return fail(SQN_ERR_INVALID_ARG, "networks is NULL");
+    sqn_status s = validate_desc(desc);
+    if (s != SQN_OK)
+        return s;
+    if (desc->D != nets->D)
+        return fail(SQN_ERR_INVALID_ARG, "desc D = %d but the networks emit D = %d", desc->D, nets->D);
+    if (!sigma_planes || !uvw_planes)
+        return fail(SQN_ERR_INVALID_ARG, "plane pointer array is NULL");
+    int device = -1;
+    if (hipGetDevice(&device) != hipSuccess)
+        return fail(SQN_ERR_DEVICE, "hipGetDevice failed");
+    if (device != nets->device)
+        return fail(SQN_ERR_INVALID_ARG, "networks live on device %d, current device is %d", nets->device,
+                    device);
+    const size_t texels = static_cast<size_t>(desc->n_p) * desc->n_p;
+    static const char* names_s[3] = {"sigma_planes[0] (xy)", "sigma_planes[1] (yz)", "sigma_planes[2] (zx)"};
+    static const char* names_u[3] = {"uvw_planes[0] (xy)", "uvw_planes[1] (yz)", "uvw_planes[2] (zx)"};
+    for (int j = 0; j < 3; ++j) {
+        if ((s = check_device_range(sigma_planes[j], texels * dtype_size(desc->sigma_dtype), names_s[j])) != SQN_OK)
+            return s;
+        if ((s = check_device_range(uvw_planes[j], texels * 3 * desc->D * dtype_size(desc->uvw_dtype),
+                                    names_u[j])) != SQN_OK)
+            return s;
+    }
+    const size_t beta_bytes = static_cast<size_t>(desc->n_theta) * desc->n_phi * desc->D
+                              * dtype_size(desc->beta_dtype);
+    if ((s = check_device_range(beta, beta_bytes, "beta")) != SQN_OK)
+        return s;
+
+    sqn::GenParams p;
+    memset(&p, 0, sizeof(p));
+    for (int j = 0; j < 3; ++j) {
+        p.pos[j] = nets->pos[j];
+        p.sigma_out[j] = sigma_planes[j];
+        p.uvw_out[j] = uvw_planes[j];
+    }
+    p.dir = nets->dir;
+    p.beta_out = beta;
+    p.n_p = desc->n_p;
+    p.n_theta = desc->n_theta;
+    p.n_phi = desc->n_phi;
+    p.D = desc->D;
+    p.pos_freq = nets->pos_freq;
+    p.dir_freq = nets->dir_freq;
+    p.pos_in = nets->pos_in;
+    p.dir_in = nets->dir_in;
+    for (int r = 0; r < 3; ++r) {
+        p.bmin[r] = desc->bbox_min[r];
+        p.bmax[r] = desc->bbox_max[r];
+    }
+    p.sigma_f16 = desc->sigma_dtype == SQN_F16;
+    p.uvw_f16 = desc->uvw_dtype == SQN_F16;
+    p.beta_f16 = desc->beta_dtype == SQN_F16;
+    hipError_t e = sqn::launch_generate(p, nets->enc_table, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return fail(SQN_ERR_DEVICE, "generation launch failed: %s", hipGetErrorString(e));
+    return SQN_OK;
+}
+
+size_t sqn_networks_device_bytes(const sqn_networks* nets) { return nets ? nets->bytes : 0; }
+
+void sqn_destroy_networks(sqn_networks* nets)
+{
+    if (!nets)
+        return;
+    if (nets->block)
+        (void)hipFree(nets->block);
+    free(nets);
 }
 
 sqn_status sqn_render(const sqn_caches* caches, const float* poses, int32_t n_poses,

@@ -93,6 +93,36 @@ constexpr int32_t lin_pad(int32_t n)
 constexpr int32_t lin_stride(int32_t D) { return lin_pad(9 * D + 3); }
 constexpr int32_t lin_stride_generic(int32_t D) { return lin_pad(10 * D + 3); }
 
+// ---- cache generation (generate.hip) ----------------------------------------
+
+// Most hidden layers a network may have.
+constexpr int32_t kMaxHidden = 16;
+
+// One network on the device: per layer (hidden layers, then the head) the
+// weights in MFMA fragment order (binary16) and the binary32 biases.
+struct GenNet {
+    const void* frag[kMaxHidden + 1];
+    const float* bias[kMaxHidden + 1];
+    int32_t n_hidden;
+    int32_t out_tiles;        // 32-row tiles of the head
+};
+
+struct GenParams {
+    GenNet pos[3];            // F_pos^xy, F_pos^yz, F_pos^zx (256 units)
+    GenNet dir;               // F_dir (128 units)
+    int32_t n_p, n_theta, n_phi, D;
+    int32_t pos_freq, dir_freq, pos_in, dir_in;
+    float bmin[3], bmax[3];
+    void* sigma_out[3];
+    void* uvw_out[3];
+    void* beta_out;
+    int32_t sigma_f16, uvw_f16, beta_f16;
+};
+
+// Encoding tables (3 n_p (1 + 2 pos_freq) binary16 values of scratch in
+// enc_table), then the position and direction kernels, on `stream`.
+hipError_t launch_generate(const GenParams& p, _Float16* enc_table, hipStream_t stream);
+
 // Workgroup geometry: 256 threads = 4 wave64; with L lanes per ray a wave
 // holds 64/L rays laid out as a wave tile of kWaveW(L) x kWaveH(L) pixels and
 // a workgroup covers 2 x 2 wave tiles.
