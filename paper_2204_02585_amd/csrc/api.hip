@@ -527,10 +527,13 @@ struct NetImage {
     int out_tiles = 0;
 };
 
-// head_rows: physical row -> source output row of the head
-NetImage make_image(const sqn_mlp_desc* m, int width, int in_steps, const std::vector<int>& head_rows,
-                    int out_tiles)
+// head_rows: physical row -> source output row of the head; the head's
+// fragments are padded with zero tiles to pad_tiles (the pipelined kernel
+// stages whole chunks of width / 32 tiles)
+NetImage make_image(const sqn_mlp_desc* m, int width, int in_steps, std::vector<int> head_rows,
+                    int out_tiles, int pad_tiles)
 {
+    head_rows.resize(static_cast<size_t>(pad_tiles) * 32, -1);
     NetImage img;
     img.n_hidden = m->n_hidden;
     img.out_tiles = out_tiles;
@@ -541,7 +544,7 @@ NetImage make_image(const sqn_mlp_desc* m, int width, int in_steps, const std::v
     for (int l = 0; l <= m->n_hidden; ++l) {
         const bool head = l == m->n_hidden;
         const int fi = l == 0 ? m->n_in : width;
-        const int t = head ? out_tiles : tiles;
+        const int t = head ? pad_tiles : tiles;
         const int steps = l == 0 ? in_steps : width / 16;
         const std::vector<int>& rows = head ? head_rows : ident;
         img.frag[l].resize(static_cast<size_t>(t) * steps * 512);
@@ -623,8 +626,8 @@ sqn_status sqn_create_networks(const sqn_mlp_desc pos[3], const sqn_mlp_desc* di
 
     NetImage img[4];
     for (int j = 0; j < 3; ++j)
-        img[j] = make_image(&pos[j], 256, 4, pos_rows, pos_tiles);
-    img[3] = make_image(dir, 128, 4, dir_rows, 1);
+        img[j] = make_image(&pos[j], 256, 4, pos_rows, pos_tiles, 8);
+    img[3] = make_image(dir, 128, 4, dir_rows, 1, 1);
 
     auto align = [](size_t x) { return (x + 255) & ~size_t{255}; };
     size_t total = 0;

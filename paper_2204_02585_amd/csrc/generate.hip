@@ -101,6 +101,90 @@ __device__ __forceinline__ void activate(const float16v (&acc)[T], const float* 
     }
 }
 
+// ---- double-buffered layers: while the matrix cores work on one chunk of
+// weights from LDS, the next chunk streams from global memory straight into
+// the other LDS buffer (global_load_lds, no registers); one barrier per
+// chunk, which also waits for those loads.
+
+struct Stage {
+    _Float16* buf[2];
+    int cur;
+};
+
+// Direct-to-LDS loads of a chunk of TMAX tiles x 4 K steps (32 KiB at 8
+// tiles; the host pads every layer of the position networks to TMAX tiles):
+// piece i = 256 k + threadIdx.x (16 bytes) lands at buf + 16 i.
+template <int TMAX>
+__device__ __forceinline__ void load_chunk(const _Float16* __restrict__ frag, _Float16* buf)
+{
+    const int wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int k = 0; k < TMAX; ++k) {
+        const int piece = 256 * k + threadIdx.x;
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const unsigned int*>(frag) + 4 * piece,
+                                         reinterpret_cast<unsigned int*>(buf) + 4 * (256 * k + 64 * wave), 16, 0, 0);
+    }
+}
+
+// One layer of KS K steps over `tiles` (<= TMAX) M-tiles for NB point
+// blocks.  The current chunk is in st.buf[st.cur] (loaded and published by
+// the last barrier); next_frag is the first chunk of the following layer
+// (after the last layer any valid chunk: loaded but never read).
+template <int TMAX, int NB, int KS>
+__device__ __forceinline__ void layer_pipe(const _Float16* __restrict__ frag, int tiles,
+                                           const half8 (&x)[NB][KS], float16v (&acc)[TMAX][NB], Stage& st,
+                                           const _Float16* next_frag)
+{
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int m = 0; m < TMAX; ++m)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+            acc[m][nb] = float16v{};
+    constexpr int NC = KS / kChunkSteps;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const bool last = c + 1 == NC;
+        load_chunk<TMAX>(last ? next_frag : frag + static_cast<size_t>(c + 1) * TMAX * kChunkSteps * kFrag,
+                         st.buf[st.cur ^ 1]);
+        const _Float16* wb = st.buf[st.cur];
+#pragma unroll
+        for (int ss = 0; ss < kChunkSteps; ++ss)
+#pragma unroll
+            for (int m = 0; m < TMAX; ++m)
+                if (m < tiles) {
+                    const half8 a = *reinterpret_cast<const half8*>(wb + ((m * kChunkSteps + ss) * 64 + lane) * 8);
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb)
+                        acc[m][nb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, x[nb][c * kChunkSteps + ss],
+                                                                            acc[m][nb], 0, 0, 0);
+                }
+        __syncthreads();
+        st.cur ^= 1;
+    }
+}
+
+template <int T, int NB>
+__device__ __forceinline__ void activate_nb(const float16v (&acc)[T][NB], const float* __restrict__ bias,
+                                            half8 (&x)[NB][2 * T])
+{
+    const int h = (threadIdx.x & 63) >> 5;
+#pragma unroll
+    for (int m = 0; m < T; ++m)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const float4 b = *reinterpret_cast<const float4*>(bias + 32 * m + 8 * g + 4 * h);
+            const float bv[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const float v = fmaxf(acc[m][nb][4 * g + q] + bv[q], 0.0f);
+                    x[nb][2 * m + (g >> 1)][4 * (g & 1) + q] = static_cast<_Float16>(v);
+                }
+        }
+}
+
 __device__ __forceinline__ void store_value(void* base, size_t idx, float v, int f16)
 {
     if (f16)
@@ -130,61 +214,76 @@ __global__ void encode_axes(GenParams P, _Float16* __restrict__ tab)
     }
 }
 
-// Position networks: blockIdx.y = plane j (xy, yz, zx); 128 points of the
-// plane's [n_p][n_p] grid per workgroup, row-major.
+// Position networks: blockIdx.y = plane j (xy, yz, zx); 256 points of the
+// plane's [n_p][n_p] grid per workgroup, row-major, kPosNB blocks of 32 per
+// wave (blocks share every weight fragment read from LDS).
+constexpr int kPosNB = 1;
+constexpr int kPosPoints = 4 * 32 * kPosNB;
+
 __global__ __launch_bounds__(256, 2) void position_kernel(GenParams P, const _Float16* __restrict__ tab)
 {
-    __shared__ __align__(16) _Float16 wbuf[8 * kChunkSteps * kFrag];
+    __shared__ __align__(16) _Float16 wbuf[2][8 * kChunkSteps * kFrag];
     const int j = blockIdx.y;
     const int lane = threadIdx.x & 63, h = lane >> 5;
     const int64_t n_pts = static_cast<int64_t>(P.n_p) * P.n_p;
-    const int64_t p_raw = static_cast<int64_t>(blockIdx.x) * 128 + (threadIdx.x >> 6) * 32 + (lane & 31);
-    const bool valid = p_raw < n_pts;
-    const int64_t p = valid ? p_raw : n_pts - 1;
-    const int ia = static_cast<int>(p / P.n_p), ib = static_cast<int>(p - static_cast<int64_t>(ia) * P.n_p);
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kPosPoints + (threadIdx.x >> 6) * (32 * kPosNB);
     // plane j = (first, second) axes (0,1), (1,2), (2,0)
     const int ax_a = j, ax_b = (j + 1) % 3;
     const int nc = 1 + 2 * P.pos_freq;
-    const _Float16* ta = tab + (static_cast<size_t>(ax_a) * P.n_p + ia) * nc;
-    const _Float16* tb = tab + (static_cast<size_t>(ax_b) * P.n_p + ib) * nc;
-
-    // input fragments: NeRF order [a, b, sin a, sin b, cos a, cos b, ...] per
-    // frequency, zero beyond n_in (64 inputs = 4 K steps)
-    half8 x0[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int f = 16 * s + kmap(h, e);
-            _Float16 v = 0;
-            if (f < 2) {
-                v = f == 0 ? ta[0] : tb[0];
-            } else if (f < P.pos_in) {
-                const int r = f - 2, k = r >> 2, t = r & 3;
-                const _Float16* src = (t & 1) ? tb : ta;
-                v = src[1 + 2 * k + (t >> 1)];
-            }
-            x0[s][e] = v;
-        }
-
     const GenNet& net = P.pos[j];
-    float16v acc[8];
-    half8 x[16];
-    layer<8, 4>(frag_of(net, 0), 8, x0, acc, wbuf);
-    activate<8>(acc, net.bias[0], x);
-    for (int l = 1; l < net.n_hidden; ++l) {
-        layer<8, 16>(frag_of(net, l), 8, x, acc, wbuf);
-        activate<8>(acc, net.bias[l], x);
+
+    // start loading the first layer's weights, then build the input
+    // fragments: NeRF order [a, b, sin a, sin b, cos a, cos b, ...] per
+    // frequency, zero beyond n_in (64 inputs = 4 K steps)
+    Stage st;
+    st.buf[0] = wbuf[0];
+    st.buf[1] = wbuf[1];
+    st.cur = 0;
+    load_chunk<8>(frag_of(net, 0), st.buf[0]);
+    int64_t pt[kPosNB];
+    half8 x0[kPosNB][4];
+#pragma unroll
+    for (int nb = 0; nb < kPosNB; ++nb) {
+        const int64_t p_raw = base + 32 * nb + (lane & 31);
+        pt[nb] = p_raw < n_pts ? p_raw : -1;
+        const int64_t p = p_raw < n_pts ? p_raw : n_pts - 1;
+        const int ia = static_cast<int>(p / P.n_p), ib = static_cast<int>(p - static_cast<int64_t>(ia) * P.n_p);
+        const _Float16* ta = tab + (static_cast<size_t>(ax_a) * P.n_p + ia) * nc;
+        const _Float16* tb = tab + (static_cast<size_t>(ax_b) * P.n_p + ib) * nc;
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int f = 16 * s + kmap(h, e);
+                _Float16 v = 0;
+                if (f < 2) {
+                    v = f == 0 ? ta[0] : tb[0];
+                } else if (f < P.pos_in) {
+                    const int r = f - 2, k = r >> 2, t = r & 3;
+                    const _Float16* src = (t & 1) ? tb : ta;
+                    v = src[1 + 2 * k + (t >> 1)];
+                }
+                x0[nb][s][e] = v;
+            }
     }
-    layer<8, 16>(frag_of(net, net.n_hidden), net.out_tiles, x, acc, wbuf);
+    __syncthreads();
+
+    float16v acc[8][kPosNB];
+    half8 x[kPosNB][16];
+    const int L = net.n_hidden;
+    layer_pipe<8, kPosNB, 4>(frag_of(net, 0), 8, x0, acc, st, frag_of(net, 1));
+    activate_nb<8, kPosNB>(acc, net.bias[0], x);
+    for (int l = 1; l < L; ++l) {
+        layer_pipe<8, kPosNB, 16>(frag_of(net, l), 8, x, acc, st, frag_of(net, l + 1));
+        activate_nb<8, kPosNB>(acc, net.bias[l], x);
+    }
+    layer_pipe<8, kPosNB, 16>(frag_of(net, L), net.out_tiles, x, acc, st, frag_of(net, L));
 
     // head: pair slot P = 16 m + 8 gg + 4 h + q sits in rows 32 m + 16 gg +
     // 4 h + q and + 8 of tile m, i.e. accumulator entries 8 gg + q and
     // 8 gg + 4 + q of this lane; slot 0 is (sigma_0, w_sigma), slot 1 + c D + d
     // is (w_c[d], c_0[d]) (Eq. 3)
-    if (!valid)
-        return;
-    const float* hb = net.bias[net.n_hidden];
+    const float* hb = net.bias[L];
     const int D = P.D;
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
@@ -196,13 +295,18 @@ __global__ __launch_bounds__(256, 2) void position_kernel(GenParams P, const _Fl
             for (int q = 0; q < 4; ++q) {
                 const int slot = 16 * m + 8 * gg + 4 * h + q;
                 const int row = 32 * m + 16 * gg + 4 * h + q;
-                const float v0 = acc[m][8 * gg + q] + hb[row];
-                const float v1 = acc[m][8 * gg + 4 + q] + hb[row + 8];
-                const float prod = v0 * v1;
-                if (slot == 0)
-                    store_value(P.sigma_out[j], static_cast<size_t>(p), prod, P.sigma_f16);
-                else if (slot <= 3 * D)
-                    store_value(P.uvw_out[j], static_cast<size_t>(p) * (3 * D) + (slot - 1), prod, P.uvw_f16);
+                const float b0 = hb[row], b1 = hb[row + 8];
+#pragma unroll
+                for (int nb = 0; nb < kPosNB; ++nb) {
+                    if (pt[nb] < 0)
+                        continue;
+                    const float prod = (acc[m][nb][8 * gg + q] + b0) * (acc[m][nb][8 * gg + 4 + q] + b1);
+                    if (slot == 0)
+                        store_value(P.sigma_out[j], static_cast<size_t>(pt[nb]), prod, P.sigma_f16);
+                    else if (slot <= 3 * D)
+                        store_value(P.uvw_out[j], static_cast<size_t>(pt[nb]) * (3 * D) + (slot - 1), prod,
+                                    P.uvw_f16);
+                }
             }
     }
 }
@@ -272,7 +376,8 @@ hipError_t launch_generate(const GenParams& p, _Float16* enc_table, hipStream_t 
     if (e != hipSuccess)
         return e;
     const int64_t n_pos = static_cast<int64_t>(p.n_p) * p.n_p;
-    position_kernel<<<dim3(static_cast<uint32_t>((n_pos + 127) / 128), 3), 256, 0, stream>>>(p, enc_table);
+    position_kernel<<<dim3(static_cast<uint32_t>((n_pos + kPosPoints - 1) / kPosPoints), 3), 256, 0, stream>>>(
+        p, enc_table);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
     const int64_t n_dir = static_cast<int64_t>(p.n_theta) * p.n_phi;
