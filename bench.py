@@ -51,20 +51,20 @@ def algorithmic_bytes(cfg, n_rays, live_inbox, occupied):
     return n_rays * per_ray + live_inbox * 3 * b_sigma + occupied * 3 * 3 * cfg.D * b
 
 
-def measured_traffic(config_name):
+def measured_traffic(config_name, kind="render"):
     """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE /
-    WRITE_SIZE passes (profiles/render_traffic_<workload>.json), scaled by
+    WRITE_SIZE passes (profiles/<kind>_traffic_<workload>.json), scaled by
     the counters of kernels of known traffic; None when no such file exists
     or the kernel source has changed since the counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"render_traffic_{config_name}.json")
-    src = os.path.join(ROOT, "paper_2204_02585_amd", "csrc", "render.hip")
+    path = os.path.join(ROOT, "profiles", f"{kind}_traffic_{config_name}.json")
+    src = os.path.join(ROOT, "paper_2204_02585_amd", "csrc", f"{kind}.hip")
     try:
         rec = json.load(open(path))
         sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
     except (OSError, ValueError):
         return None
-    if rec.get("render_hip_sha256_16") != sha:
+    if rec.get(f"{kind}_hip_sha256_16") != sha:
         return None
     return int(rec["traffic_bytes_per_launch"])
 
@@ -87,6 +87,18 @@ def cpu_baseline(scene, budget_s=12.0, max_frames=40):
     return {"value": samples / el / 1e6, "unit": "Msamples/s", "cores": threads, "kind": "oracle",
             "sample": f"{frames} full {cfg.width}x{cfg.height}x{cfg.n_samples} frame(s) of view 0, "
                       f"{el:.1f} s wall", "frames_per_s": frames / el}
+
+
+def calibration_copies(dev):
+    """Kernels of known traffic for scaling the hardware byte counters: a
+    1 GiB fill and three 1 GiB device-to-device copies."""
+    import torch
+    src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 GEN_TEXT = {
@@ -144,6 +156,8 @@ def bench_generate(args):
     f_pos, f_dir = network_flops(cfg)
     flops = n_pos * f_pos + n_dir * f_dir
     tflops = flops / (ms * 1e-3) / 1e12
+    if args.copy_calibration:
+        calibration_copies(dev)
 
     base = None
     if not args.no_cpu_baseline:
@@ -183,7 +197,8 @@ def bench_generate(args):
                    "direction_grid": [cfg.n_theta, cfg.n_phi], "D": cfg.D,
                    "position_points": n_pos, "direction_points": n_dir},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_F16_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(tflops / MFMA_F16_PEAK_TFLOPS, 4), "traffic": None,
+                     "unit": "TFLOP/s", "frac": round(tflops / MFMA_F16_PEAK_TFLOPS, 4),
+                     "traffic": measured_traffic(cfg.name, "generate"),
                      "algorithmic_flops_per_launch": int(flops), "kernel_ms_per_launch": round(ms, 4)},
         "cpu_baseline": base,
         "wall_s_timed": round(wall, 4),
@@ -269,12 +284,7 @@ def main():
     gbs = bytes_alg / (ms * 1e-3) / 1e9
 
     if args.copy_calibration:
-        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        calibration_copies(dev)
 
     base = None
     if not args.no_cpu_baseline:

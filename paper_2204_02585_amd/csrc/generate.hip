@@ -149,16 +149,27 @@ __device__ __forceinline__ void layer_pipe(const _Float16* __restrict__ frag, in
                          st.buf[st.cur ^ 1]);
         const _Float16* wb = st.buf[st.cur];
 #pragma unroll
-        for (int ss = 0; ss < kChunkSteps; ++ss)
+        for (int ss = 0; ss < kChunkSteps; ++ss) {
+            // fragment reads of the step ahead of its products, so each wait
+            // covers several reads; the other wave on the SIMD fills it
+            half8 a[TMAX];
+#pragma unroll
+            for (int m = 0; m < TMAX; ++m)
+                a[m] = *reinterpret_cast<const half8*>(wb + ((m * kChunkSteps + ss) * 64 + lane) * 8);
 #pragma unroll
             for (int m = 0; m < TMAX; ++m)
                 if (m < tiles) {
-                    const half8 a = *reinterpret_cast<const half8*>(wb + ((m * kChunkSteps + ss) * 64 + lane) * 8);
 #pragma unroll
                     for (int nb = 0; nb < NB; ++nb)
-                        acc[m][nb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, x[nb][c * kChunkSteps + ss],
+                        acc[m][nb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[m], x[nb][c * kChunkSteps + ss],
                                                                             acc[m][nb], 0, 0, 0);
                 }
+            // in halves: four reads, four products (bounds the registers)
+            __builtin_amdgcn_sched_group_barrier(0x100, TMAX / 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, TMAX / 2 * NB, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, TMAX / 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, TMAX / 2 * NB, 0);
+        }
         __syncthreads();
         st.cur ^= 1;
     }
