@@ -63,7 +63,8 @@ class _Scene(ctypes.Structure):
 class _Camera(ctypes.Structure):
     _fields_ = [("fx", ctypes.c_float), ("fy", ctypes.c_float),
                 ("cx", ctypes.c_float), ("cy", ctypes.c_float),
-                ("width", ctypes.c_int32), ("height", ctypes.c_int32)]
+                ("width", ctypes.c_int32), ("height", ctypes.c_int32),
+                ("ndc_near", ctypes.c_float), ("pad", ctypes.c_int32)]
 
 
 RAY_DTYPE = np.dtype([("rgb", np.float64, (3,)), ("depth", np.float64),
@@ -129,14 +130,16 @@ def render(sigma: Sequence[np.ndarray], uvw: Sequence[np.ndarray], beta: np.ndar
            poses: np.ndarray, intrinsics: dict, near: float, far: float, n_samples: int,
            bbox_min, bbox_max, t_eps: float = 1e-4, stratified: bool = False,
            seed: int = 0, ray_ids: Optional[np.ndarray] = None,
-           n_threads: Optional[int] = None, decoder=None) -> np.ndarray:
+           n_threads: Optional[int] = None, decoder=None, ndc_near: float = 0.0) -> np.ndarray:
     """Render rays on the CPU; returns a structured array of RAY_DTYPE
     (rgb, depth, acc, tau_end, stop, n_inbox, n_occ, hash), one per ray,
     in ray-id order ((b*H + v)*W + u) or in the order of `ray_ids`.
 
     decoder: None for Eq. 4, or an object with w_sigma [3 D_sigma],
     b_sigma, w_uvw [3][D][3D] and b_uvw [3][D] for Eq. 5; then each
-    sigma[j] is [n_p][n_p][D_sigma]."""
+    sigma[j] is [n_p][n_p][D_sigma].  ndc_near > 0 marches in normalized
+    device coordinates with that near plane (forward-facing captures);
+    near/far are then the NDC ray parameters, usually 0 and 1."""
     lib = _load()
     sigma = [np.ascontiguousarray(a) for a in sigma]
     uvw = [np.ascontiguousarray(a) for a in uvw]
@@ -179,7 +182,8 @@ def render(sigma: Sequence[np.ndarray], uvw: Sequence[np.ndarray], beta: np.ndar
         sc.b_uvw = b_uvw.ctypes.data
 
     cam = _Camera(float(intrinsics["fx"]), float(intrinsics["fy"]), float(intrinsics["cx"]),
-                  float(intrinsics["cy"]), int(intrinsics["width"]), int(intrinsics["height"]))
+                  float(intrinsics["cy"]), int(intrinsics["width"]), int(intrinsics["height"]),
+                  float(ndc_near), 0)
     total = poses.shape[0] * cam.width * cam.height
     if ray_ids is None:
         ids_ptr, n = None, total
@@ -210,4 +214,5 @@ def render_scene(scene, ray_ids=None, n_threads=None, n_samples=None, t_eps=None
                   t_eps=cfg.t_eps if t_eps is None else t_eps,
                   stratified=cfg.stratified if stratified is None else stratified,
                   seed=scene.seed, ray_ids=ray_ids, n_threads=n_threads,
-                  decoder=getattr(scene, "decoder", None))
+                  decoder=getattr(scene, "decoder", None),
+                  ndc_near=getattr(scene, "ndc_near", 0.0))

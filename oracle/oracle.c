@@ -135,6 +135,47 @@ static void alt_logits(const oracle_scene* sc, const size_t rec[3], const double
     }
 }
 
+/* ---- normalized device coordinates ------------------------------------- */
+
+/* Forward-facing captures (LLFF) are marched in the normalized device
+ * coordinates of a pinhole camera looking down -z with near plane n: a world
+ * point (x, y, z), z < 0, maps to
+ *   x' = -(fx / (W/2)) x / z,  y' = -(fy / (H/2)) y / z,  z' = 1 + 2 n / z,
+ * so the frustum from z = -n to infinity becomes [-1, 1]^3 and straight
+ * lines stay straight.  The ray o + t d is first moved to its point on the
+ * near plane (t_s = -(n + o_z) / d_z); in these coordinates it is then
+ * o' + t' d' with t' in [0, 1) from the near plane to infinity:
+ *   o' = (-(sx) o_x/o_z, -(sy) o_y/o_z, 1 + 2n/o_z),
+ *   d' = (-(sx) (d_x/d_z - o_x/o_z), -(sy) (d_y/d_z - o_y/o_z), -2n/o_z),
+ * sx = fx / (W/2), sy = fy / (H/2).  A ray with d_z >= 0 never reaches the
+ * near plane and has no samples.  Binary32, one rounding per operation, in
+ * the order written.  Returns 0 for a ray without samples. */
+static int ndc_ray(const oracle_camera* cam, float o[3], float d[3])
+{
+    const float n = cam->ndc_near;
+    if (!(d[2] < 0.0f))
+        return 0;
+    float ts = -(n + o[2]) / d[2];
+    float os[3];
+    for (int r = 0; r < 3; ++r) {
+        float td = ts * d[r];
+        os[r] = o[r] + td;
+    }
+    const float sx = cam->fx / (0.5f * (float)cam->width);
+    const float sy = cam->fy / (0.5f * (float)cam->height);
+    const float oxz = os[0] / os[2], oyz = os[1] / os[2];
+    const float dxz = d[0] / d[2], dyz = d[1] / d[2];
+    const float n2 = 2.0f * n;
+    const float n2z = n2 / os[2];
+    o[0] = -(sx * oxz);
+    o[1] = -(sy * oyz);
+    o[2] = 1.0f + n2z;
+    d[0] = -(sx * (dxz - oxz));
+    d[1] = -(sy * (dyz - oyz));
+    d[2] = -n2z;
+    return 1;
+}
+
 /* ---- one ray ------------------------------------------------------------ */
 
 typedef struct {
@@ -235,12 +276,15 @@ static void render_ray(const job_t* J, int64_t ray_id, oracle_ray* out)
         d[r] = (pa + pb) - P[4 * r + 2];
         o[r] = P[4 * r + 3];
     }
-    float d00 = d[0] * d[0], d11 = d[1] * d[1], d22 = d[2] * d[2];
-    float dnorm = sqrtf((d00 + d11) + d22);
-
-    /* Direction weights, once per ray. */
+    /* Direction weights, once per ray, from the world direction. */
     double beta[64];
     lookup_beta(sc, d, beta);
+
+    int no_samples = 0;
+    if (cam->ndc_near > 0.0f && !ndc_ray(cam, o, d))
+        no_samples = 1;
+    float d00 = d[0] * d[0], d11 = d[1] * d[1], d22 = d[2] * d[2];
+    float dnorm = sqrtf((d00 + d11) + d22);
 
     int64_t tau = 0;          /* sum_{j<i} sigma_j delta_j in units of 2^-32 */
     uint32_t hash = 2166136261u;
@@ -257,7 +301,7 @@ static void render_ray(const job_t* J, int64_t ray_id, oracle_ray* out)
         float t_next = (i + 1 < N) ? sample_t(J, ray_id, i + 1) : J->far_t;
 
         float p[3];
-        int inside = 1;
+        int inside = !no_samples;
         for (int r = 0; r < 3; ++r) {
             float td = t * d[r];
             p[r] = o[r] + td;

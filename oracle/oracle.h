@@ -9,7 +9,9 @@
  * What it computes, per pixel ray (SqueezeNeRF Sec. 3.1 Eq. 1-2, Sec. 3.2
  * Eq. 4, Sec. 3.3, Sec. 3.4):
  *   - a pinhole ray from the camera centre through the pixel centre
- *     (Sec. 3.1);
+ *     (Sec. 3.1); for forward-facing captures (the LLFF scenes of Sec. 4)
+ *     optionally mapped to normalized device coordinates, the NeRF
+ *     convention the paper inherits;
  *   - N samples between the near and far planes (Sec. 3.1), uniform or
  *     stratified with a seeded SplitMix64 offset per bin;
  *   - nearest-neighbour lookup of sigma^j and (u^j, v^j, w^j) in the three
@@ -69,6 +71,9 @@ typedef struct {
 typedef struct {
     float fx, fy, cx, cy;   /* pinhole intrinsics, pixels                     */
     int32_t width, height;
+    float ndc_near;         /* > 0: march in normalized device coordinates    */
+                            /* of the forward-facing camera (see oracle.c)    */
+    int32_t pad;
 } oracle_camera;
 
 typedef struct {

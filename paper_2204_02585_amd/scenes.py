@@ -65,6 +65,8 @@ class Config:
     t_eps: float = 1e-4
     focal: Optional[float] = None  # default 1.25 * width
     sigma_channels: int = 0        # 0: Eq. 4 product of scalar sigma^j; > 0: Eq. 5 linear map
+    forward: bool = False          # forward-facing capture marched in NDC (LLFF-shaped)
+    sigma_dtype: Optional[str] = None  # storage of sigma^j if it differs from dtype
 
     @property
     def fx(self) -> float:
@@ -96,6 +98,13 @@ CONFIGS = {
     # "SqueezeNeRF (alt)" decoder (Eq. 5, D_sigma = 12) on the paper shape
     "alt": Config("alt", 6, 800, 800, 192, 256, 8, 128, 128, "f16", 64, 50.0, 0.1, 0.4,
                   sigma_channels=12),
+    # forward-facing (LLFF-shaped): 504x378, the paper's 512 cache with its
+    # precisions (sigma fp32, uvw and beta fp16), n_d = 32, 256 samples in NDC
+    "llff": Config("llff", 9, 504, 378, 256, 512, 8, 32, 32, "f16", 64, 50.0, 0.05, 0.25,
+                   focal=0.8 * 504, forward=True, sigma_dtype="f32"),
+    # a small forward-facing case the oracle renders in full
+    "llff_tiny": Config("llff_tiny", 10, 48, 36, 64, 64, 8, 16, 16, "f32", 48, 50.0, 0.05, 0.25,
+                        focal=0.8 * 48, forward=True),
     # the alt decoder at the paper's alt cache size (n_p = 512, n_d = 256)
     "alt512": Config("alt512", 7, 800, 800, 192, 512, 8, 256, 256, "f16", 64, 50.0, 0.1, 0.4,
                      sigma_channels=12),
@@ -291,6 +300,7 @@ class Scene:
     bbox_max: tuple = BOX_MAX
     seed: int = 0
     decoder: Optional[LinearDecoder] = None   # set for the linear (alt) decoder
+    ndc_near: float = 0.0                     # > 0: rays marched in NDC
 
     @property
     def intrinsics(self):
@@ -313,19 +323,72 @@ def make_scene(name_or_config, n_poses: Optional[int] = None) -> Scene:
         cfg = dataclasses.replace(cfg, n_poses=n_poses)
     n = cfg.number
     dt = np_dtype(cfg.dtype)
+    sdt = np_dtype(cfg.sigma_dtype or cfg.dtype)
+    if cfg.forward:
+        return _forward_scene(cfg)
     blobs = make_blobs(cfg.n_blobs, cfg.sigma_max, cfg.r_min, cfg.r_max, 1000 + n)
     decoder = None
     if cfg.sigma_channels > 0:
-        sigma = bake_linear_sigma_planes(cfg.n_p, blobs, cfg.sigma_channels, dt)
+        sigma = bake_linear_sigma_planes(cfg.n_p, blobs, cfg.sigma_channels, sdt)
         decoder = linear_decoder(cfg.sigma_channels, cfg.D, cfg.sigma_max, 6000 + n)
     else:
-        sigma = bake_sigma_planes(cfg.n_p, blobs, dt)
+        sigma = bake_sigma_planes(cfg.n_p, blobs, sdt)
     rng_uvw = np.random.Generator(np.random.PCG64(2000 + n))
     uvw = [uniform_pm1((cfg.n_p, cfg.n_p, 3 * cfg.D), dt, rng_uvw) for _ in range(3)]
     rng_beta = np.random.Generator(np.random.PCG64(3000 + n))
     beta = uniform_pm1((cfg.n_theta, cfg.n_phi, cfg.D), dt, rng_beta)
     poses = single_pose() if cfg.n_poses == 1 else spiral_poses(cfg.n_poses)
     return Scene(cfg, sigma, uvw, beta, poses, seed=4000 + n, decoder=decoder)
+
+
+NDC_BOX = ((-1.0, -1.0, -1.0), (1.0, 1.0, 1.0))
+NDC_NEAR = 1.0
+
+
+def forward_pose(dx: float = 0.0, dy: float = 0.0, yaw_deg: float = 0.0, pitch_deg: float = 0.0):
+    """Camera near the origin looking down -z (the frame of a forward-facing
+    capture), moved by (dx, dy) and turned by small yaw / pitch angles."""
+    cy, sy = math.cos(math.radians(yaw_deg)), math.sin(math.radians(yaw_deg))
+    cp, sp = math.cos(math.radians(pitch_deg)), math.sin(math.radians(pitch_deg))
+    Ry = np.array([[cy, 0, sy], [0, 1, 0], [-sy, 0, cy]])
+    Rx = np.array([[1, 0, 0], [0, cp, -sp], [0, sp, cp]])
+    P = np.zeros((3, 4))
+    P[:, :3] = Ry @ Rx
+    P[:, 3] = (dx, dy, 0.0)
+    return P.astype(np.float32)
+
+
+def forward_poses(n: int, seed: int = 5100) -> np.ndarray:
+    """n forward-facing views: small seeded offsets (+-0.1) and turns (+-5 deg);
+    the first is the reference view at the origin."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    out = [forward_pose()]
+    for _ in range(n - 1):
+        out.append(forward_pose(*rng.uniform(-0.1, 0.1, 2), *rng.uniform(-5.0, 5.0, 2)))
+    return np.stack(out)
+
+
+def _forward_scene(cfg: Config) -> Scene:
+    """Forward-facing (LLFF-shaped) inputs: the caches span the NDC box
+    [-1, 1]^3 of a camera looking down -z with near plane 1 (samples t' in
+    [0, 1) from the near plane to infinity).  Blobs sit in NDC at x', y' in
+    [-0.7, 0.7] and z' in [-0.6, 0.95] (world depths 1.25 to 40)."""
+    n = cfg.number
+    dt = np_dtype(cfg.dtype)
+    sdt = np_dtype(cfg.sigma_dtype or cfg.dtype)
+    rng = np.random.Generator(np.random.PCG64(1000 + n))
+    centre = np.stack([rng.uniform(-0.7, 0.7, cfg.n_blobs), rng.uniform(-0.7, 0.7, cfg.n_blobs),
+                       rng.uniform(-0.6, 0.95, cfg.n_blobs)], axis=1)
+    blobs = Blobs(centre, rng.uniform(cfg.r_min, cfg.r_max, cfg.n_blobs), float(cfg.sigma_max))
+    lo, hi = NDC_BOX
+    sigma = bake_sigma_planes(cfg.n_p, blobs, sdt, bmin=lo, bmax=hi)
+    rng_uvw = np.random.Generator(np.random.PCG64(2000 + n))
+    uvw = [uniform_pm1((cfg.n_p, cfg.n_p, 3 * cfg.D), dt, rng_uvw) for _ in range(3)]
+    rng_beta = np.random.Generator(np.random.PCG64(3000 + n))
+    beta = uniform_pm1((cfg.n_theta, cfg.n_phi, cfg.D), dt, rng_beta)
+    poses = forward_poses(cfg.n_poses)
+    return Scene(cfg, sigma, uvw, beta, poses, near=0.0, far=1.0, bbox_min=lo, bbox_max=hi,
+                 seed=4000 + n, ndc_near=NDC_NEAR)
 
 
 # --------------------------------------------------------------------------

@@ -418,6 +418,94 @@ def test_alt_density_summation_order(parts, bias, n_occ, q_units):
 
 
 # --------------------------------------------------------------------------
+# forward-facing captures: rays in normalized device coordinates (NDC)
+# --------------------------------------------------------------------------
+# A pinhole camera looking down -z with near plane n maps a world point
+# (x, y, z) to (-(fx/(W/2)) x/z, -(fy/(H/2)) y/z, 1 + 2n/z); the frustum
+# beyond the near plane becomes [-1, 1]^3.  For a camera at the origin the
+# ray of pixel (u, v) becomes the segment x' = (u + 1/2 - cx)/(W/2),
+# y' = -(v + 1/2 - cy)/(H/2), z' = -1 + 2 t' (t' in [0, 1)), of length 2.
+
+NDC_BOX = ((-1.0, -1.0, -1.0), (1.0, 1.0, 1.0))
+
+
+def _ndc_render(sigma_planes, pose, intr, N, t_eps=0.0):
+    n_p = sigma_planes[0].shape[0]
+    return oracle.render(sigma_planes, uvw_const(n_p, 1, [(0, 0, 0)] * 3), beta_const(0.0),
+                         pose, intr, 0.0, 1.0, N, *NDC_BOX, t_eps=t_eps, ndc_near=1.0)
+
+
+def test_ndc_camera_at_origin_uniform_density():
+    """Every ray of a camera at the origin has length 2 inside the box, so
+    opacity 1 - exp(-2 sigma) and depth sum_i e^(-i q)(1 - e^-q) i/N with
+    q = 2 sigma / N (t' is the depth parameter)."""
+    sig, N = 0.6, 32
+    intr = dict(fx=6.0, fy=6.0, cx=4.0, cy=3.0, width=8, height=6)
+    out = _ndc_render(const_planes(2, (sig, 1.0, 1.0)), np.eye(3, 4, dtype=np.float32)[None], intr, N)
+    q = 2.0 * sig / N
+    depth = sum(math.exp(-i * q) * (1 - math.exp(-q)) * (i / N) for i in range(N))
+    assert np.all(out["stop"] == N) and np.all(out["n_inbox"] == N) and np.all(out["n_occ"] == N)
+    assert np.all(np.abs(out["acc"] - (1.0 - math.exp(-2.0 * sig))) < 1e-6)
+    assert np.all(np.abs(out["depth"] - depth) < 1e-6)
+
+
+@pytest.mark.parametrize("axis", ["x", "y"])
+def test_ndc_pixel_columns_and_rows(axis):
+    """17 nodes over [-1, 1] (spacing 1/8), W = H = 8, c = 4: pixel u has
+    x' = (u - 7/2)/4, i.e. grid coordinate 2u + 1, so node 15 is pixel
+    column u = 7 only; y' = -(v - 7/2)/4 puts node 15 on the top row v = 0.
+    Density only on that node line of the xy plane lights exactly that
+    column (or row), along the whole ray (x' and y' stay constant)."""
+    n_p = 17
+    planes = const_planes(n_p, (0.0, 1.0, 1.0))
+    if axis == "x":
+        planes[0][15, :] = 2.0
+    else:
+        planes[0][:, 15] = 2.0
+    intr = dict(fx=8.0, fy=8.0, cx=4.0, cy=4.0, width=8, height=8)
+    out = _ndc_render(planes, np.eye(3, 4, dtype=np.float32)[None], intr, 16).reshape(8, 8)
+    lit = np.zeros((8, 8), bool)
+    if axis == "x":
+        lit[:, 7] = True
+    else:
+        lit[0, :] = True
+    assert np.all(out["n_occ"][lit] == 16) and np.all(out["n_occ"][~lit] == 0)
+    assert np.allclose(out["acc"][lit], 1.0 - math.exp(-4.0), atol=1e-6)
+
+
+def test_ndc_translated_camera_parallax():
+    """Camera at (3/8, 0, 0), one pixel on the axis (fx = 1, W = 1, so
+    fx/(W/2) = 2): the ray starts at x' = 2 * 3/8 = 3/4 on the near plane
+    and converges to the vanishing point x' = 0 at t' = 1:
+    x'(t') = (3/4)(1 - t'), z'(t') = -1 + 2 t'.  With 9 nodes (spacing 1/4)
+    and density on nodes x' >= 1/2, samples t' = i/8 are occupied while
+    x' >= 3/8 (ties round up): i = 0..4 at nodes ix = 7, 7, 6, 6, 6,
+    iy = 4, iz = 0..4; |d'| = sqrt(9/16 + 4)."""
+    n_p = 9
+    planes = const_planes(n_p, (0.0, 1.0, 1.0))
+    planes[0][6:, :] = 1.0
+    pose = np.eye(3, 4, dtype=np.float32)[None].copy()
+    pose[0, 0, 3] = 0.375
+    r = _ndc_render(planes, pose, ONE_PIXEL, 8)[0]
+    assert r["n_occ"] == 5 and r["n_inbox"] == 8
+    words = []
+    for i, ix in enumerate([7, 7, 6, 6, 6]):
+        words += [i, ix, 4, i]
+    assert r["hash"] == fnv1a(words)
+    q = math.sqrt(0.5625 + 4.0) / 8
+    assert abs(r["acc"] - (1 - math.exp(-5 * q))) < 1e-6
+
+
+def test_ndc_ray_pointing_away_is_empty():
+    """A ray with d_z >= 0 never reaches the near plane: no samples."""
+    planes = const_planes(2, (1.0, 1.0, 1.0))
+    pose = np.zeros((1, 3, 4), np.float32)
+    pose[0, :, :3] = np.diag([-1.0, 1.0, -1.0])       # looks down +z
+    r = _ndc_render(planes, pose, ONE_PIXEL, 8)[0]
+    assert r["n_inbox"] == 0 and r["n_occ"] == 0 and r["stop"] == 8 and r["acc"] == 0
+
+
+# --------------------------------------------------------------------------
 # Eq. 1: closed forms for uniform density
 # --------------------------------------------------------------------------
 
@@ -552,7 +640,7 @@ def test_image_orientation():
 # invariants on the seeded synthetic scenes
 # --------------------------------------------------------------------------
 
-@pytest.fixture(scope="module", params=["tiny", "tiny_alt"])
+@pytest.fixture(scope="module", params=["tiny", "tiny_alt", "llff_tiny"])
 def tiny_scene(request):
     from paper_2204_02585_amd import scenes
     return scenes.make_scene(request.param)
@@ -591,6 +679,7 @@ def test_early_termination_changes_colour_by_at_most_eps(tiny_scene):
 def test_ray_subset_matches_full_render(tiny_scene):
     sc = tiny_scene
     full = oracle.render_scene(sc)
-    ids = np.array([0, 17, 2049, 4095, 1234], dtype=np.int64)
+    total = full.size
+    ids = np.array([0, 17, total // 2 + 1, total - 1, total // 3], dtype=np.int64)
     sub = oracle.render_scene(sc, ray_ids=ids)
     assert np.array_equal(sub, full[ids])
