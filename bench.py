@@ -32,6 +32,7 @@ WORKLOAD_TEXT = {
     "large": "800x800 image, 192 uniform samples/ray, k=1024 D=8 fp16 caches, 384x384 fp16 direction cache, 64 blobs sigma_max 200",
     "batch": "100 spiral views of 800x800, 192 uniform samples/ray, k=256 D=8 fp16 caches, 128x128 fp16 direction cache",
     "stress": "1920x1080 image, 384 stratified samples/ray, k=2048 D=16 fp16 caches, 512x512 fp16 direction cache, 256 blobs",
+    "llff": "forward-facing (LLFF-shaped), rays in NDC: 504x378 image, 256 uniform samples/ray, the paper's 512 cache (sigma fp32, uvw fp16, D=8), 32x32 fp16 direction cache, 64 blobs in the NDC box",
     "alt": "Eq. 5 linear decoder (D_sigma=12): 800x800 image, 192 uniform samples/ray, k=256 D=8 fp16 caches, 128x128 fp16 direction cache, 64 blobs",
     "alt512": "Eq. 5 linear decoder (D_sigma=12) at the paper's alt cache size: 800x800 image, 192 uniform samples/ray, k=512 D=8 fp16 caches, 256x256 fp16 direction cache, 64 blobs",
 }
@@ -46,7 +47,7 @@ def algorithmic_bytes(cfg, n_rays, live_inbox, occupied):
     ray from cache and not counted); per live occupied sample the three uvw
     records (3D values)."""
     b = 2 if cfg.dtype == "f16" else 4
-    b_sigma = 4 if cfg.sigma_channels > 0 else b
+    b_sigma = 4 if (cfg.sigma_channels > 0 or (cfg.sigma_dtype or cfg.dtype) == "f32") else 2
     per_ray = 4 * cfg.D * b + 16
     return n_rays * per_ray + live_inbox * 3 * b_sigma + occupied * 3 * 3 * cfg.D * b
 

@@ -277,6 +277,25 @@ size_t sqn_networks_device_bytes(const sqn_networks* nets);
 /* Free the networks; NULL is a no-op. */
 void sqn_destroy_networks(sqn_networks* nets);
 
+/* Ray space of later renders with this handle.  ndc_near = 0 (the default):
+ * world rays as above.  ndc_near > 0: forward-facing captures (the LLFF
+ * scenes the paper evaluates, Sec. 4), marched as in NeRF in the normalized
+ * device coordinates of the pinhole camera looking down -z with near plane
+ * ndc_near: a world point (x, y, z) maps to (-(fx/(W/2)) x/z,
+ * -(fy/(H/2)) y/z, 1 + 2 ndc_near/z), so the frustum beyond the near plane
+ * is [-1, 1]^3 (the caches' box).  Each ray is moved to its point on the
+ * near plane, t_s = -(ndc_near + o_z)/d_z, and becomes o' + t' d'; near and
+ * far of sqn_render are then t' bounds (0 and 1 span near plane to
+ * infinity), delta_i uses |d'|, depth_out is sum w_i t'_i, and beta is
+ * still looked up along the world direction.  Rays with d_z >= 0 have no
+ * samples.  Binary32, one rounding per operation:
+ *   o' = (-(sx (o_x/o_z)), -(sy (o_y/o_z)), 1 + (2n)/o_z),
+ *   d' = (-(sx (d_x/d_z - o_x/o_z)), -(sy (d_y/d_z - o_y/o_z)), -((2n)/o_z)),
+ *   sx = fx/(0.5 W), sy = fy/(0.5 H), o after the move.
+ * Not thread-safe against concurrent renders with the handle.
+ * Errors: SQN_ERR_INVALID_ARG (NULL, negative or non-finite). */
+sqn_status sqn_set_ndc(sqn_caches* caches, float ndc_near);
+
 /* Bytes of device memory the handle owns. */
 size_t sqn_cache_device_bytes(const sqn_caches* caches);
 

@@ -19,7 +19,7 @@ SQN_OK, SQN_ERR_INVALID_ARG, SQN_ERR_OUT_OF_MEMORY, SQN_ERR_DEVICE, SQN_ERR_UNSU
 SQN_F32, SQN_F16 = 0, 1
 
 EXPORTS = ("sqn_create_caches", "sqn_create_linear_caches", "sqn_render", "sqn_render_stats",
-           "sqn_set_lanes_per_ray", "sqn_set_empty_space_skipping", "sqn_cache_device_bytes",
+           "sqn_set_lanes_per_ray", "sqn_set_empty_space_skipping", "sqn_set_ndc", "sqn_cache_device_bytes",
            "sqn_destroy", "sqn_status_string", "sqn_last_error", "sqn_create_networks",
            "sqn_generate_caches", "sqn_networks_device_bytes", "sqn_destroy_networks")
 
@@ -92,6 +92,8 @@ def _load() -> ctypes.CDLL:
     lib.sqn_set_lanes_per_ray.argtypes = [vp, i32]
     lib.sqn_set_empty_space_skipping.restype = ctypes.c_int
     lib.sqn_set_empty_space_skipping.argtypes = [vp, i32]
+    lib.sqn_set_ndc.restype = ctypes.c_int
+    lib.sqn_set_ndc.argtypes = [vp, f32]
     lib.sqn_cache_device_bytes.restype = ctypes.c_size_t
     lib.sqn_cache_device_bytes.argtypes = [vp]
     lib.sqn_destroy.restype = None
@@ -209,6 +211,11 @@ class Caches:
         """Leaps over empty space (default) or a dense march."""
         _check(lib.sqn_set_empty_space_skipping(self.handle, 1 if enable else 0))
 
+    def set_ndc(self, ndc_near: float) -> None:
+        """Forward-facing rays in normalized device coordinates with near
+        plane ndc_near (> 0), or world rays (0)."""
+        _check(lib.sqn_set_ndc(self.handle, float(ndc_near)))
+
     def close(self) -> None:
         if self._h:
             lib.sqn_destroy(self._h)
@@ -264,6 +271,8 @@ def caches_from_scene(scene, device="cuda", t_eps=None, stratified=None, stream=
                     t_eps=cfg.t_eps if t_eps is None else t_eps,
                     stratified=cfg.stratified if stratified is None else stratified,
                     seed=scene.seed, stream=stream, decoder=getattr(scene, "decoder", None))
+    if getattr(scene, "ndc_near", 0.0) > 0.0:
+        caches.set_ndc(scene.ndc_near)
     return caches
 
 

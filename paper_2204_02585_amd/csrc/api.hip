@@ -25,6 +25,7 @@ struct sqn_caches {
     int64_t tau_eps;         // floor(-ln(eps) 2^32)
     int32_t lanes;           // lanes per ray, 0 = chosen per call
     int32_t skip;            // empty-space leaps (one lane per ray)
+    float ndc_near;          // > 0: forward-facing rays in normalized device coordinates
     // linear (Eq. 5) decoder
     int32_t linear;          // 1: sigma[j] hold per-plane partial sums
     int32_t d_sigma;
@@ -276,6 +277,7 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
     p.lin_w = h->lin_w;
     // rows per ray in LDS; the kernels for D = 8 and 16 use lin_stride(D)
     p.lin_stride = sqn::lin_stride_generic(h->desc.D);
+    p.ndc_near = h->ndc_near;
     p.leap_margin = 1e-3f;
     const int tw = sqn::kTileW(p.lanes), th = sqn::kTileH(p.lanes);
     p.tiles_x = (in->width + tw - 1) / tw;
@@ -805,6 +807,16 @@ sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes)
     if (caches->linear && lanes == 1)
         return fail(SQN_ERR_UNSUPPORTED, "the linear decoder renders with four lanes per ray");
     caches->lanes = lanes;
+    return SQN_OK;
+}
+
+sqn_status sqn_set_ndc(sqn_caches* caches, float ndc_near)
+{
+    if (!caches)
+        return fail(SQN_ERR_INVALID_ARG, "caches is NULL");
+    if (!(ndc_near >= 0.0f) || !isfinite(ndc_near))
+        return fail(SQN_ERR_INVALID_ARG, "ndc_near = %g must be finite and >= 0", static_cast<double>(ndc_near));
+    caches->ndc_near = ndc_near;
     return SQN_OK;
 }
 

@@ -226,6 +226,40 @@ __device__ __forceinline__ float sample_t(const RenderParams& P, bool stratified
     return P.near_t + xd;
 }
 
+// Normalized device coordinates of a camera looking down -z with near plane
+// n (forward-facing captures): a world point (x, y, z) maps to
+// (-(fx/(W/2)) x/z, -(fy/(H/2)) y/z, 1 + 2n/z), the frustum beyond the near
+// plane to [-1, 1]^3.  The ray is moved to its point on the near plane,
+// t_s = -(n + o_z)/d_z, and becomes o' + t' d' with t' in [0, 1) up to
+// infinity.  Binary32, one rounding per operation, in this order.  A ray
+// with d_z >= 0 never reaches the near plane: returns false (no samples).
+__device__ __forceinline__ bool ndc_ray(const RenderParams& P, float o[3], float d[3])
+{
+    const float n = P.ndc_near;
+    if (!(d[2] < 0.0f))
+        return false;
+    const float ts = -(n + o[2]) / d[2];
+    float os[3];
+#pragma unroll
+    for (int r = 0; r < 3; ++r) {
+        const float td = ts * d[r];
+        os[r] = o[r] + td;
+    }
+    const float sx = P.fx / (0.5f * static_cast<float>(P.width));
+    const float sy = P.fy / (0.5f * static_cast<float>(P.height));
+    const float oxz = os[0] / os[2], oyz = os[1] / os[2];
+    const float dxz = d[0] / d[2], dyz = d[1] / d[2];
+    const float n2 = 2.0f * n;
+    const float n2z = n2 / os[2];
+    o[0] = -(sx * oxz);
+    o[1] = -(sy * oyz);
+    o[2] = 1.0f + n2z;
+    d[0] = -(sx * (dxz - oxz));
+    d[1] = -(sy * (dyz - oyz));
+    d[2] = -n2z;
+    return true;
+}
+
 // Conservative sample-index range [i0, i1] of the scene box: every sample
 // outside it fails the exact in-box test.  Face crossings are widened by
 // 1e-5 relative (far beyond the few-ulp misplacement of the binary32
@@ -609,7 +643,7 @@ constexpr int waves_per_simd(int record_bytes)
 // SKIP: leap over runs of samples that one plane's distance field proves
 // empty (with L lanes per ray, the run that starts at the chunk's last
 // sample decides where the next chunk starts).
-template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool LIN>
+template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool LIN, bool NDC>
 __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, int32_t u,
                                            int32_t v, int32_t lane, float* const beta, float* const lin)
 {
@@ -635,12 +669,7 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
         d[r] = (pa + pb) - pm[4 * r + 2];
         o[r] = pm[4 * r + 3];
     }
-    const float d00 = d[0] * d[0], d11 = d[1] * d[1], d22 = d[2] * d[2];
-    const float dn = sqrtf((d00 + d11) + d22);
-
-    int32_t i0, i1;
-    clip_to_box(P, o, d, i0, i1);
-
+    // direction weights from the world direction
     if constexpr (LIN) {
         // beta goes to the ray's LDS row (the L lanes write equal values)
         lookup_beta<DC, L, 1>(P, d, s, DC > 0 ? lin : lin + 9 * P.D + 3);
@@ -648,6 +677,22 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
         fold_decoder<DC, L>(P, s, lin);
     } else {
         lookup_beta<DC, L, kBlockThreads>(P, d, s, beta);
+    }
+
+    // forward-facing captures march in normalized device coordinates
+    bool no_samples = false;
+    if constexpr (NDC)
+        no_samples = !ndc_ray(P, o, d);
+    const float d00 = d[0] * d[0], d11 = d[1] * d[1], d22 = d[2] * d[2];
+    const float dn = sqrtf((d00 + d11) + d22);
+
+    int32_t i0, i1;
+    clip_to_box(P, o, d, i0, i1);
+    if constexpr (NDC) {
+        if (no_samples) {
+            i0 = 1;
+            i1 = 0;
+        }
     }
 
     const int32_t n_p = P.n_p;
@@ -898,7 +943,7 @@ constexpr int occupancy()
     return regs < by_lds ? regs : (by_lds < 1 ? 1 : by_lds);
 }
 
-template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool LIN>
+template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool LIN, bool NDC>
 __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN>())) void render_kernel(const RenderParams P)
 {
     // beta of every lane's ray, component-major so that a wave-wide read of
@@ -926,21 +971,29 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN>())) void ren
             constexpr int32_t stride = DC > 0 ? lin_stride(DC) : 0;
             lin = lin_smem + (threadIdx.x / 4) * (DC > 0 ? stride : P.lin_stride);
         }
-        render_ray<ST, UT, DC, STATS, L, SKIP, LIN>(P, view, u, v, lane,
+        render_ray<ST, UT, DC, STATS, L, SKIP, LIN, NDC>(P, view, u, v, lane,
                                                     LIN ? beta_smem : beta_smem + threadIdx.x, lin);
     }
 }
 
-template <typename ST, typename UT, int DC, int L, bool SKIP, bool LIN>
-hipError_t launch_shape(const RenderParams& p, bool stats, hipStream_t stream)
+template <typename ST, typename UT, int DC, int L, bool SKIP, bool LIN, bool NDC>
+hipError_t launch_ray_space(const RenderParams& p, bool stats, hipStream_t stream)
 {
     const dim3 grid(static_cast<uint32_t>(p.n_groups));
     const dim3 block(kBlockThreads);
     if (stats)
-        render_kernel<ST, UT, DC, true, L, SKIP, LIN><<<grid, block, 0, stream>>>(p);
+        render_kernel<ST, UT, DC, true, L, SKIP, LIN, NDC><<<grid, block, 0, stream>>>(p);
     else
-        render_kernel<ST, UT, DC, false, L, SKIP, LIN><<<grid, block, 0, stream>>>(p);
+        render_kernel<ST, UT, DC, false, L, SKIP, LIN, NDC><<<grid, block, 0, stream>>>(p);
     return hipGetLastError();
+}
+
+// world rays, or forward-facing rays in normalized device coordinates
+template <typename ST, typename UT, int DC, int L, bool SKIP, bool LIN>
+hipError_t launch_shape(const RenderParams& p, bool stats, hipStream_t stream)
+{
+    return p.ndc_near > 0.0f ? launch_ray_space<ST, UT, DC, L, SKIP, LIN, true>(p, stats, stream)
+                             : launch_ray_space<ST, UT, DC, L, SKIP, LIN, false>(p, stats, stream);
 }
 
 template <typename ST, typename UT, int DC>

@@ -47,6 +47,7 @@ struct RenderParams {
     float b_sigma;            // density bias
     const float* lin_w;       // [9D + 3][D]: rows c*3D + e of W_c^T, then b_u, b_v, b_w
     int32_t lin_stride;       // LDS floats per ray of the folded weights
+    float ndc_near;           // > 0: rays marched in normalized device coordinates
 };
 
 // Launch one render over all views on `stream`; `stats` selects the variant
