@@ -362,7 +362,42 @@ __device__ __forceinline__ void lookup_beta(const RenderParams& P, const float d
         return grp_sum<L>(acc);
     };
     // component k goes to beta_lds[k * BS]
-    if constexpr (DC > 0) {
+    if constexpr (DC == 8) {
+        // each corner record (D contiguous values) in 16-byte loads (at
+        // D = 16 this measured slower than per-component loads)
+        float acc[DC];
+#pragma unroll
+        for (int k = 0; k < DC; ++k)
+            acc[k] = 0.0f;
+#pragma unroll
+        for (int c = 0; c < 4; c += L) {
+            const int corner = c + (L == 1 ? 0 : s);
+            const float w = wgt[corner];
+            if (P.beta_f16) {
+#pragma unroll
+                for (int q = 0; q < DC / 8; ++q) {
+                    const uint4 raw = load_at<uint4>(P.beta, texel[corner] * (DC * 2u) + 16u * q);
+                    _Float16 h[8];
+                    __builtin_memcpy(h, &raw, 16);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        acc[8 * q + e] = fmaf(w, widen(h[e]), acc[8 * q + e]);
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < DC / 4; ++q) {
+                    const float4 v = load_at<float4>(P.beta, texel[corner] * (DC * 4u) + 16u * q);
+                    acc[4 * q + 0] = fmaf(w, v.x, acc[4 * q + 0]);
+                    acc[4 * q + 1] = fmaf(w, v.y, acc[4 * q + 1]);
+                    acc[4 * q + 2] = fmaf(w, v.z, acc[4 * q + 2]);
+                    acc[4 * q + 3] = fmaf(w, v.w, acc[4 * q + 3]);
+                }
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < DC; ++k)
+            beta_lds[k * BS] = grp_sum<L>(acc[k]);
+    } else if constexpr (DC > 0) {
 #pragma unroll
         for (int k = 0; k < DC; ++k)
             beta_lds[k * BS] = component(k);
