@@ -31,6 +31,8 @@ struct sqn_caches {
     int32_t d_sigma;
     float b_sigma;
     const float* lin_w;      // [9D + 3][D] folded radiance weights and biases
+    const uint8_t* cell_dist;  // [m^3] cell distances (Eq. 5 leaps)
+    int32_t cell_shift, cell_m;
 };
 
 // Device copy of the networks for cache generation.
@@ -278,6 +280,9 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
     // rows per ray in LDS; the kernels for D = 8 and 16 use lin_stride(D)
     p.lin_stride = sqn::lin_stride_generic(h->desc.D);
     p.ndc_near = h->ndc_near;
+    p.cell_dist = h->cell_dist;
+    p.cell_shift = h->cell_shift;
+    p.cell_m = h->cell_m;
     p.leap_margin = 1e-3f;
     const int tw = sqn::kTileW(p.lanes), th = sqn::kTileH(p.lanes);
     p.tiles_x = (in->width + tw - 1) / tw;
@@ -325,6 +330,9 @@ sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec
                               * dtype_size(desc->beta_dtype);
     const size_t lin_rows = 9 * static_cast<size_t>(D) + 3;
     const size_t lin_bytes = linear ? lin_rows * D * sizeof(float) : 0;
+    const int32_t cell_shift = sqn::linear_cell_shift(desc->n_p);
+    const int32_t cell_m = sqn::linear_cells(desc->n_p);
+    const size_t cells = linear ? static_cast<size_t>(cell_m) * cell_m * cell_m : 0;
     static const char* names_s[3] = {"sigma_planes[0] (xy)", "sigma_planes[1] (yz)", "sigma_planes[2] (zx)"};
     static const char* names_u[3] = {"uvw_planes[0] (xy)", "uvw_planes[1] (yz)", "uvw_planes[2] (zx)"};
     for (int j = 0; j < 3; ++j) {
@@ -350,6 +358,8 @@ sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec
     total += align(beta_bytes);
     off_lin = total;
     total += align(lin_bytes);
+    const size_t off_cells = total;
+    total += align(cells);
 
     // temporary buffers of the preparation, freed before returning
     size_t work_total = 0;
@@ -363,6 +373,14 @@ sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec
     work_total += align(6 * static_cast<size_t>(desc->n_p) * sizeof(float));
     const size_t w_ws = work_total;
     work_total += align(3 * static_cast<size_t>(ds) * sizeof(float));
+    const size_t w_cmax = work_total;
+    work_total += align(3 * static_cast<size_t>(cell_m) * cell_m * sizeof(float));
+    const size_t w_clive = work_total;
+    work_total += align(cells);
+    const size_t w_cf = work_total;
+    work_total += align(cells * sizeof(uint16_t));
+    const size_t w_cf2 = work_total;
+    work_total += align(cells * sizeof(uint16_t));
 
     // host-side parameters of the linear decoder: W_sigma, and the radiance
     // weights transposed so that row c*3D + e holds W_c[0..D)[e], followed
@@ -416,6 +434,10 @@ sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec
     pw.dist = reinterpret_cast<uint16_t*>(work + w_dist);
     pw.maxima = reinterpret_cast<float*>(work + w_max);
     pw.w_sigma = reinterpret_cast<float*>(work + w_ws);
+    pw.cell_max = reinterpret_cast<float*>(work + w_cmax);
+    pw.cell_live = reinterpret_cast<uint8_t*>(work + w_clive);
+    pw.cell_f = reinterpret_cast<uint16_t*>(work + w_cf);
+    pw.cell_f2 = reinterpret_cast<uint16_t*>(work + w_cf2);
 
     void* packed[3];
     for (int j = 0; j < 3; ++j) {
@@ -432,6 +454,9 @@ sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec
         if (e == hipSuccess)
             e = sqn::prepare_linear_planes(sigma_planes, desc->sigma_dtype, desc->n_p, ds, dec->b_sigma,
                                            packed, pw, st);
+        if (e == hipSuccess)
+            e = sqn::prepare_linear_cells(packed, desc->n_p, dec->b_sigma, cell_shift, cell_m,
+                                          reinterpret_cast<uint8_t*>(base + off_cells), pw, st);
     } else {
         for (int j = 0; j < 3 && e == hipSuccess; ++j)
             e = sqn::prepare_sigma_plane(sigma_planes[j], desc->sigma_dtype, desc->n_p, packed[j], pw, st);
@@ -460,6 +485,9 @@ sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec
         h->d_sigma = ds;
         h->b_sigma = dec->b_sigma;
         h->lin_w = reinterpret_cast<const float*>(base + off_lin);
+        h->cell_dist = reinterpret_cast<const uint8_t*>(base + off_cells);
+        h->cell_shift = cell_shift;
+        h->cell_m = cell_m;
     }
     *out = h;
     g_last_error.clear();

@@ -210,7 +210,124 @@ __global__ void set_distance(const uint16_t* __restrict__ dist, uint2* __restric
         packed[i].y = static_cast<uint32_t>(dist[i]);
 }
 
+// ---- cell grid of the linear decoder ---------------------------------------
+
+// max of s^j over the g x g texels of each cell of plane j (cells [m][m]).
+__global__ void cell_max(const uint2* __restrict__ packed, int32_t n_p, int32_t shift, int32_t m,
+                         float* __restrict__ out)
+{
+    const int32_t cb = blockIdx.x * blockDim.x + threadIdx.x;
+    const int32_t ca = blockIdx.y;
+    if (cb >= m)
+        return;
+    const int32_t g = 1 << shift;
+    const int32_t a1 = min(n_p, (ca + 1) * g), b1 = min(n_p, (cb + 1) * g);
+    float mx = -INFINITY;
+    for (int32_t a = ca * g; a < a1; ++a)
+        for (int32_t b = cb * g; b < b1; ++b)
+            mx = fmaxf(mx, __uint_as_float(packed[static_cast<uint32_t>(a) * n_p + b].x));
+    out[ca * m + cb] = mx;
+}
+
+// live[(cx m + cy) m + cz]: the bound ((M_xy + M_yz) + M_zx) + b is not <= 0.
+__global__ void cell_live(const float* __restrict__ cmax, int32_t m, float b_sigma, uint8_t* __restrict__ live)
+{
+    const int32_t cz = blockIdx.x * blockDim.x + threadIdx.x;
+    const int32_t cy = blockIdx.y, cx = blockIdx.z;
+    if (cz >= m)
+        return;
+    const float* mxy = cmax;
+    const float* myz = cmax + m * m;
+    const float* mzx = cmax + 2 * m * m;
+    float bound = mxy[cx * m + cy] + myz[cy * m + cz];
+    bound = bound + mzx[cz * m + cx];
+    bound = bound + b_sigma;
+    live[(static_cast<uint32_t>(cx) * m + cy) * m + cz] = (bound <= 0.0f) ? 0 : 1;
+}
+
+// Distance along z (innermost) to the nearest live cell, capped at cap + 1.
+__global__ void cell_dist_z(const uint8_t* __restrict__ live, uint16_t* __restrict__ f, int32_t m, int32_t cap)
+{
+    const int32_t row = blockIdx.x * blockDim.x + threadIdx.x;
+    if (row >= m * m)
+        return;
+    const uint32_t base = static_cast<uint32_t>(row) * m;
+    const int32_t far = cap + 1;
+    int32_t last = -(1 << 30);
+    for (int32_t z = 0; z < m; ++z) {
+        if (live[base + z])
+            last = z;
+        f[base + z] = static_cast<uint16_t>(min(far, z - last));
+    }
+    last = 1 << 30;
+    for (int32_t z = m - 1; z >= 0; --z) {
+        if (live[base + z])
+            last = z;
+        const int32_t fz = min(far, last - z);
+        if (fz < f[base + z])
+            f[base + z] = static_cast<uint16_t>(fz);
+    }
+}
+
+// One separable Chebyshev pass along axis y (stride m) or x (stride m^2):
+// out = min over k of max(|k|, in at offset k), capped at cap + 1.
+__global__ void cell_dist_pass(const uint16_t* __restrict__ in, uint16_t* __restrict__ out, int32_t m,
+                               int32_t along_x, int32_t cap)
+{
+    const int32_t cz = blockIdx.x * blockDim.x + threadIdx.x;
+    const int32_t cy = blockIdx.y, cx = blockIdx.z;
+    if (cz >= m)
+        return;
+    const int32_t pos = along_x ? cx : cy;
+    const int32_t stride = along_x ? m * m : m;
+    const uint32_t idx = (static_cast<uint32_t>(cx) * m + cy) * m + cz;
+    int32_t best = in[idx];
+    for (int32_t k = 1; k < best && k <= cap; ++k) {
+        if (pos - k >= 0)
+            best = min(best, max(k, static_cast<int32_t>(in[idx - k * stride])));
+        if (pos + k < m)
+            best = min(best, max(k, static_cast<int32_t>(in[idx + k * stride])));
+    }
+    out[idx] = static_cast<uint16_t>(min(best, cap + 1));
+}
+
+__global__ void cell_store(const uint16_t* __restrict__ f, uint8_t* __restrict__ dist, uint32_t n, int32_t cap)
+{
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n)
+        dist[i] = static_cast<uint8_t>(min(static_cast<int32_t>(f[i]), cap));
+}
+
 }  // namespace
+
+hipError_t prepare_linear_cells(const void* const packed[3], int32_t n_p, float b_sigma, int32_t shift,
+                                int32_t m, uint8_t* cell_dist, const PrepareWork& work, hipStream_t stream)
+{
+    hipError_t e = hipSuccess;
+    for (int j = 0; j < 3; ++j) {
+        cell_max<<<dim3((m + 63) / 64, m), 64, 0, stream>>>(static_cast<const uint2*>(packed[j]), n_p, shift, m,
+                                                            work.cell_max + j * m * m);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+    }
+    const dim3 cells((m + 63) / 64, m, m);
+    cell_live<<<cells, 64, 0, stream>>>(work.cell_max, m, b_sigma, work.cell_live);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    const int32_t cap = 255;
+    cell_dist_z<<<dim3((m * m + 63) / 64), 64, 0, stream>>>(work.cell_live, work.cell_f, m, cap);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    cell_dist_pass<<<cells, 64, 0, stream>>>(work.cell_f, work.cell_f2, m, 0, cap);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    cell_dist_pass<<<cells, 64, 0, stream>>>(work.cell_f2, work.cell_f, m, 1, cap);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    const uint32_t n = static_cast<uint32_t>(m) * m * m;
+    cell_store<<<dim3((n + 255) / 256), 256, 0, stream>>>(work.cell_f, cell_dist, n, cap);
+    return hipGetLastError();
+}
 
 hipError_t prepare_sigma_plane(const void* sigma, int sigma_dtype, int32_t n_p, void* packed,
                                const PrepareWork& work, hipStream_t stream)

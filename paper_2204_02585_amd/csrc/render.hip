@@ -645,6 +645,33 @@ __device__ __forceinline__ int32_t leap_target(const RenderParams& P, int j, uin
     return static_cast<int32_t>(fminf(fmaxf(f, lo), hi));
 }
 
+// First sample index a leap may land on after sample i, whose node indices
+// lie in cell cc of the 3-D cell grid (cells of G x G x G nodes) at
+// Chebyshev distance D > 0 (in cells) from every cell that may hold
+// sigma > 0.  Every sample whose cell stays within distance D - 1 is empty:
+// along each axis the node index stays inside cells cc - (D-1) .. cc + (D-1),
+// i.e. g in [G (cc - D + 1) - 1/2, G (cc + D) - 1/2), while g = g0 + t ds
+// moves affinely in t.  Margins as in leap_target.
+__device__ __forceinline__ int32_t leap_cells(const RenderParams& P, uint32_t D, const uint32_t cc[3],
+                                              const float g0[3], const float inv_ds[3], const float ds[3],
+                                              float margin, int32_t i)
+{
+    const float G = static_cast<float>(1 << P.cell_shift);
+    const float Df = static_cast<float>(D);
+    float t_exit = INFINITY;
+#pragma unroll
+    for (int r = 0; r < 3; ++r) {
+        const float c = static_cast<float>(cc[r]);
+        const float bound = ds[r] > 0.0f ? G * (c + Df) - 0.5f - margin : G * (c - Df + 1.0f) - 0.5f + margin;
+        const float tr = (bound - g0[r]) * inv_ds[r];
+        if (ds[r] != 0.0f)
+            t_exit = fminf(t_exit, tr);
+    }
+    const float f = floorf((t_exit - P.near_t) * P.inv_dt) - 1.0f;
+    const float lo = static_cast<float>(i + 1), hi = static_cast<float>(P.n_samples);
+    return static_cast<int32_t>(fminf(fmaxf(f, lo), hi));
+}
+
 // Map the hardware workgroup id to a tile.  Workgroups are dealt
 // round-robin over the 8 XCDs.  SQN_XCD_BLOCK = 0: each XCD receives one
 // contiguous run of tiles; K > 0: runs of K consecutive tiles are dealt to
@@ -787,29 +814,42 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
             ix = nearest_node(p[0], P.bmin[0], P.scale[0], hi_node);
             iy = nearest_node(p[1], P.bmin[1], P.scale[1], hi_node);
             iz = nearest_node(p[2], P.bmin[2], P.scale[2], hi_node);
-            float sxy, syz, szx;
-            uint32_t dxy, dyz, dzx;
-            SigmaRecord<ST>::load(P.sigma[0], __umul24(ix, n_p) + iy, sxy, dxy);
-            SigmaRecord<ST>::load(P.sigma[1], __umul24(iy, n_p) + iz, syz, dyz);
-            SigmaRecord<ST>::load(P.sigma[2], __umul24(iz, n_p) + ix, szx, dzx);
-            if constexpr (LIN) {
-                // Eq. 5 on the folded per-plane partial sums
-                float pre = sxy + syz;
-                pre = pre + szx;
-                pre = pre + P.b_sigma;
-                sigma = pre > 0.0f ? pre : 0.0f;
-            } else {
-                // Eq. 4
-                float prod = sxy * syz;
-                prod = prod * szx;
-                sigma = fmaxf(0.0f, prod);
+            // Eq. 5: a sample in an empty cell of the 3-D cell grid has
+            // sigma = 0 without reading the planes
+            bool dead = false;
+            if constexpr (LIN && SKIP) {
+                const uint32_t cc[3] = {ix >> P.cell_shift, iy >> P.cell_shift, iz >> P.cell_shift};
+                const uint32_t cd = P.cell_dist[(cc[0] * P.cell_m + cc[1]) * P.cell_m + cc[2]];
+                if (cd != 0) {
+                    dead = true;
+                    leap = leap_cells(P, cd, cc, g0, inv_ds, ds, leap_margin, i);
+                }
             }
-            if constexpr (SKIP) {
-                const uint32_t dmax = max(dxy, max(dyz, dzx));
-                if (dmax != 0) {
-                    const int j = (dxy == dmax) ? 0 : ((dyz == dmax) ? 1 : 2);
-                    const uint32_t c[3] = {ix, iy, iz};
-                    leap = leap_target(P, j, dmax, c, g0, inv_ds, ds, leap_margin, i);
+            if (!dead) {
+                float sxy, syz, szx;
+                uint32_t dxy, dyz, dzx;
+                SigmaRecord<ST>::load(P.sigma[0], __umul24(ix, n_p) + iy, sxy, dxy);
+                SigmaRecord<ST>::load(P.sigma[1], __umul24(iy, n_p) + iz, syz, dyz);
+                SigmaRecord<ST>::load(P.sigma[2], __umul24(iz, n_p) + ix, szx, dzx);
+                if constexpr (LIN) {
+                    // Eq. 5 on the folded per-plane partial sums
+                    float pre = sxy + syz;
+                    pre = pre + szx;
+                    pre = pre + P.b_sigma;
+                    sigma = pre > 0.0f ? pre : 0.0f;
+                } else {
+                    // Eq. 4
+                    float prod = sxy * syz;
+                    prod = prod * szx;
+                    sigma = fmaxf(0.0f, prod);
+                }
+                if constexpr (SKIP) {
+                    const uint32_t dmax = max(dxy, max(dyz, dzx));
+                    if (dmax != 0) {
+                        const int j = (dxy == dmax) ? 0 : ((dyz == dmax) ? 1 : 2);
+                        const uint32_t c[3] = {ix, iy, iz};
+                        leap = leap_target(P, j, dmax, c, g0, inv_ds, ds, leap_margin, i);
+                    }
                 }
             }
         }

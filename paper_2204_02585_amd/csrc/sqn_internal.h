@@ -48,6 +48,11 @@ struct RenderParams {
     const float* lin_w;       // [9D + 3][D]: rows c*3D + e of W_c^T, then b_u, b_v, b_w
     int32_t lin_stride;       // LDS floats per ray of the folded weights
     float ndc_near;           // > 0: rays marched in normalized device coordinates
+    // Eq. 5: 3-D grid of cells of cell_g^3 nodes, cell_m per axis, holding
+    // the capped Chebyshev distance (cells) to the nearest cell that may
+    // hold sigma > 0
+    const uint8_t* cell_dist;
+    int32_t cell_shift, cell_m;   // cell side 2^cell_shift nodes
 };
 
 // Launch one render over all views on `stream`; `stats` selects the variant
@@ -66,6 +71,10 @@ struct PrepareWork {
     uint16_t* dist;       // [n_p^2] capped Chebyshev distances
     float* maxima;        // [6][n_p] row / column maxima of the partial sums
     float* w_sigma;       // [3 d_sigma] density weights (linear decoder)
+    float* cell_max;      // [3][m][m] per-plane cell maxima (linear decoder)
+    uint8_t* cell_live;   // [m^3]
+    uint16_t* cell_f;     // [m^3] partial distances
+    uint16_t* cell_f2;    // [m^3]
 };
 
 // Pack sigma plane j (n_p x n_p of sigma_dtype, device memory) into
@@ -82,6 +91,27 @@ hipError_t prepare_sigma_plane(const void* sigma, int sigma_dtype, int32_t n_p, 
 hipError_t prepare_linear_planes(const void* const sigma[3], int sigma_dtype, int32_t n_p,
                                  int32_t d_sigma, float b_sigma, void* const packed[3],
                                  const PrepareWork& work, hipStream_t stream);
+
+// Cell grid of the linear decoder (after prepare_linear_planes): cells of
+// g x g x g nodes (g = 2^shift), m = ceil(n_p / g) per axis; a cell is empty when
+// ((M_xy + M_yz) + M_zx) + b_sigma <= 0 with M_j the largest partial sum of
+// plane j over the cell's footprint (binary32 addition is monotone), and
+// cell_dist[(cx m + cy) m + cz] receives the capped Chebyshev distance in
+// cells to the nearest cell not so marked.  work.cell_max holds 3 m^2
+// floats, work.cell_live m^3 bytes, work.cell_f / cell_g2 m^3 uint16 each.
+hipError_t prepare_linear_cells(const void* const packed[3], int32_t n_p, float b_sigma, int32_t shift,
+                                int32_t m, uint8_t* cell_dist, const PrepareWork& work, hipStream_t stream);
+
+// Cell side 2^shift for an n_p grid: the smallest power of two >= 2 that
+// leaves at most 128 cells per axis.
+constexpr int32_t linear_cell_shift(int32_t n_p)
+{
+    int32_t s = 1;
+    while (((n_p + (1 << s) - 1) >> s) > 128)
+        ++s;
+    return s;
+}
+constexpr int32_t linear_cells(int32_t n_p) { return (n_p + (1 << linear_cell_shift(n_p)) - 1) >> linear_cell_shift(n_p); }
 
 // Per-ray LDS floats of the folded Eq. 5 radiance weights: n values padded
 // to 4 (mod 8) words so that 16 rays' 16-byte reads spread over the banks.
