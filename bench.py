@@ -90,6 +90,34 @@ def cpu_baseline(scene, budget_s=12.0, max_frames=40):
                       f"{el:.1f} s wall", "frames_per_s": frames / el}
 
 
+def memory_ceilings(cache_bytes):
+    """Ceilings of the memory levels the render kernel's gathers are served
+    from, measured on this GPU by libsqn_probe.so: streaming reads of a
+    2 MiB buffer (held by each XCD's L2), a 128 MiB buffer (held by the
+    MALL) and a 4 GiB buffer (HBM), and random 64-byte-record gathers over
+    buffers of those sizes and of the workload's cache size.  GB/s."""
+    import ctypes
+    from paper_2204_02585_amd import build as _build
+    lib = ctypes.CDLL(_build.PROBE_PATH)
+    lib.sqn_probe_stream.argtypes = [ctypes.c_uint64, ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
+    lib.sqn_probe_gather.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.POINTER(ctypes.c_float)]
+    ms = ctypes.c_float()
+    out = {"stream_gbs": {}, "gather64_gbs": {}}
+    for label, nbytes, passes in (("2MiB", 2 << 20, 2000), ("128MiB", 128 << 20, 16), ("4GiB", 4 << 30, 1)):
+        if lib.sqn_probe_stream(nbytes, passes, ctypes.byref(ms)) != 0:
+            raise RuntimeError("stream probe failed")
+        out["stream_gbs"][label] = round(nbytes * passes / (ms.value * 1e-3) / 1e9, 1)
+    cache_label = f"cache {cache_bytes / 1e6:.1f} MB"
+    n_rec = 1 << 24
+    for label, nbytes in (("2MiB", 2 << 20), (cache_label, (int(cache_bytes) + 63) // 64 * 64),
+                          ("128MiB", 128 << 20), ("4GiB", 4 << 30)):
+        if lib.sqn_probe_gather(nbytes, n_rec, ctypes.byref(ms)) != 0:
+            raise RuntimeError("gather probe failed")
+        out["gather64_gbs"][label] = round(n_rec * 64 / (ms.value * 1e-3) / 1e9, 1)
+    out["cache_label"] = cache_label
+    return out
+
+
 def calibration_copies(dev):
     """Kernels of known traffic for scaling the hardware byte counters: a
     1 GiB fill and three 1 GiB device-to-device copies."""
@@ -159,6 +187,12 @@ def bench_generate(args):
     tflops = flops / (ms * 1e-3) / 1e12
     if args.copy_calibration:
         calibration_copies(dev)
+    ceilings = None
+    if not args.no_ceilings:
+        print("[bench] memory ceilings", file=sys.stderr, flush=True)
+        ceilings = memory_ceilings(scene.cache_nbytes())
+        g = ceilings["gather64_gbs"][ceilings.pop("cache_label")]
+        ceilings["render_vs_gather64_at_cache_size"] = round(gbs / g, 4)
 
     base = None
     if not args.no_cpu_baseline:
@@ -219,6 +253,8 @@ def main():
     ap.add_argument("--dense", action="store_true",
                     help="march every sample (no leaps over empty space)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the memory-level ceiling probes")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB device-to-device 3 times (a kernel "
@@ -286,6 +322,12 @@ def main():
 
     if args.copy_calibration:
         calibration_copies(dev)
+    ceilings = None
+    if not args.no_ceilings:
+        print("[bench] memory ceilings", file=sys.stderr, flush=True)
+        ceilings = memory_ceilings(scene.cache_nbytes())
+        g = ceilings["gather64_gbs"][ceilings.pop("cache_label")]
+        ceilings["render_vs_gather64_at_cache_size"] = round(gbs / g, 4)
 
     base = None
     if not args.no_cpu_baseline:
@@ -324,6 +366,7 @@ def main():
                      "algorithmic_bytes_per_launch": int(bytes_alg),
                      "kernel_ms_per_launch": round(ms, 5)},
         "cpu_baseline": base,
+        "ceilings": ceilings,
         "wall_s_timed": round(wall, 4),
     }
     print(json.dumps(out), flush=True)

@@ -11,6 +11,9 @@ CSRC = os.path.join(PKG, "csrc")
 LIB_PATH = os.path.join(PKG, "libsqn.so")
 SOURCES = [os.path.join(CSRC, "api.hip"), os.path.join(CSRC, "render.hip"),
            os.path.join(CSRC, "prepare.hip"), os.path.join(CSRC, "generate.hip")]
+# memory-level ceilings for the benchmark's roofline (not part of the render ABI)
+PROBE_PATH = os.path.join(PKG, "libsqn_probe.so")
+PROBE_SOURCES = [os.path.join(CSRC, "probe.hip")]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",
@@ -34,16 +37,21 @@ HIPCC_FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
-    """Compile libsqn.so (always recompiles)."""
+def _compile(sources, path, verbose):
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = LIB_PATH + ".tmp"
+    tmp = path + ".tmp"
     cmd = [hipcc, *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-           "-o", tmp, *SOURCES]
+           "-o", tmp, *sources]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB_PATH)
+    os.replace(tmp, path)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile libsqn.so and libsqn_probe.so (always recompiles)."""
+    _compile(SOURCES, LIB_PATH, verbose)
+    _compile(PROBE_SOURCES, PROBE_PATH, verbose)
     return LIB_PATH
 
 

@@ -117,3 +117,19 @@ def test_linear_decoder_validation_before_device_calls(lib):
     # a valid decoder reaches the plane checks
     assert create(dec()) == lib.SQN_ERR_INVALID_ARG and "sigma_planes" in lib.last_error()
     assert not out
+
+
+def test_probe_library_exports_and_rejects_bad_sizes():
+    """The benchmark's memory-ceiling probes (libsqn_probe.so) load and
+    reject sizes they cannot measure before touching the device."""
+    from paper_2204_02585_amd import build
+    raw = ctypes.CDLL(build.PROBE_PATH)
+    raw.sqn_probe_stream.argtypes = [ctypes.c_uint64, ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
+    raw.sqn_probe_gather.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.POINTER(ctypes.c_float)]
+    ms = ctypes.c_float()
+    assert raw.sqn_probe_stream(15, 1, ctypes.byref(ms)) == 1
+    assert raw.sqn_probe_stream(1 << 20, 0, ctypes.byref(ms)) == 1
+    assert raw.sqn_probe_stream(1 << 20, 1, None) == 1
+    assert raw.sqn_probe_gather(100, 1, ctypes.byref(ms)) == 1
+    assert raw.sqn_probe_gather(1 << 20, 0, ctypes.byref(ms)) == 1
+    assert raw.sqn_probe_gather(64 << 32, 1, ctypes.byref(ms)) == 1
