@@ -187,12 +187,6 @@ def bench_generate(args):
     tflops = flops / (ms * 1e-3) / 1e12
     if args.copy_calibration:
         calibration_copies(dev)
-    ceilings = None
-    if not args.no_ceilings:
-        print("[bench] memory ceilings", file=sys.stderr, flush=True)
-        ceilings = memory_ceilings(scene.cache_nbytes())
-        g = ceilings["gather64_gbs"][ceilings.pop("cache_label")]
-        ceilings["render_vs_gather64_at_cache_size"] = round(gbs / g, 4)
 
     base = None
     if not args.no_cpu_baseline:
