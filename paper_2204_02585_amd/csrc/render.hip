@@ -624,22 +624,24 @@ struct SigmaRecord<float> {
 // below c + D - 1/2 (or above c - D + 1/2 moving down).  The bound is pulled
 // in by `margin` texels (the binary32 position and rounding error of g) and
 // the result by one sample, so every skipped sample is inside the square.
+// inv_ds[r] = 1 / ds[r], +inf for ds = 0, so that an axis the ray does not
+// move along never ends the run (a non-positive distance to the bound there
+// gives -inf or NaN, i.e. no leap or the other axis: never a longer one);
+// its sign tells the direction.
 __device__ __forceinline__ int32_t leap_target(const RenderParams& P, int j, uint32_t D, const uint32_t c[3],
-                                               const float g0[3], const float inv_ds[3], const float ds[3],
-                                               float margin, int32_t i)
+                                               const float g0[3], const float inv_ds[3], float margin, int32_t i)
 {
     const float h = static_cast<float>(D) - 0.5f - margin;
-    float t_exit = INFINITY;
+    float t[3];
 #pragma unroll
     for (int r = 0; r < 3; ++r) {
-        // plane 0 (xy) uses axes 0, 1; plane 1 (yz) 1, 2; plane 2 (zx) 2, 0
-        const bool used = (r == j) || (r == (j + 1) % 3);
-        const float cr = static_cast<float>(c[r]);
-        const float bound = ds[r] > 0.0f ? cr + h : cr - h;
-        const float tr = (bound - g0[r]) * inv_ds[r];
-        if (used && ds[r] != 0.0f)
-            t_exit = fminf(t_exit, tr);
+        // c + h or c - h
+        const float bound = static_cast<float>(c[r]) + copysignf(h, inv_ds[r]);
+        t[r] = (bound - g0[r]) * inv_ds[r];
     }
+    // plane 0 (xy) uses axes 0, 1; plane 1 (yz) 1, 2; plane 2 (zx) 2, 0
+    const float t01 = fminf(t[0], t[1]), t12 = fminf(t[1], t[2]), t20 = fminf(t[2], t[0]);
+    const float t_exit = j == 0 ? t01 : (j == 1 ? t12 : t20);
     const float f = floorf((t_exit - P.near_t) * P.inv_dt) - 1.0f;
     const float lo = static_cast<float>(i + 1), hi = static_cast<float>(P.n_samples);
     return static_cast<int32_t>(fminf(fmaxf(f, lo), hi));
@@ -651,10 +653,9 @@ __device__ __forceinline__ int32_t leap_target(const RenderParams& P, int j, uin
 // sigma > 0.  Every sample whose cell stays within distance D - 1 is empty:
 // along each axis the node index stays inside cells cc - (D-1) .. cc + (D-1),
 // i.e. g in [G (cc - D + 1) - 1/2, G (cc + D) - 1/2), while g = g0 + t ds
-// moves affinely in t.  Margins as in leap_target.
+// moves affinely in t.  Margins and zero components as in leap_target.
 __device__ __forceinline__ int32_t leap_cells(const RenderParams& P, uint32_t D, const uint32_t cc[3],
-                                              const float g0[3], const float inv_ds[3], const float ds[3],
-                                              float margin, int32_t i)
+                                              const float g0[3], const float inv_ds[3], float margin, int32_t i)
 {
     const float G = static_cast<float>(1 << P.cell_shift);
     const float Df = static_cast<float>(D);
@@ -662,10 +663,8 @@ __device__ __forceinline__ int32_t leap_cells(const RenderParams& P, uint32_t D,
 #pragma unroll
     for (int r = 0; r < 3; ++r) {
         const float c = static_cast<float>(cc[r]);
-        const float bound = ds[r] > 0.0f ? G * (c + Df) - 0.5f - margin : G * (c - Df + 1.0f) - 0.5f + margin;
-        const float tr = (bound - g0[r]) * inv_ds[r];
-        if (ds[r] != 0.0f)
-            t_exit = fminf(t_exit, tr);
+        const float bound = inv_ds[r] > 0.0f ? G * (c + Df) - 0.5f - margin : G * (c - Df + 1.0f) - 0.5f + margin;
+        t_exit = fminf(t_exit, (bound - g0[r]) * inv_ds[r]);
     }
     const float f = floorf((t_exit - P.near_t) * P.inv_dt) - 1.0f;
     const float lo = static_cast<float>(i + 1), hi = static_cast<float>(P.n_samples);
@@ -760,14 +759,14 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
     const int32_t n_p = P.n_p;
     const float hi_node = static_cast<float>(n_p - 1);
     // grid coordinate of each axis as an affine function of t, for leaps
-    float g0[3], ds[3], inv_ds[3];
+    float g0[3], inv_ds[3];
     float leap_margin = 0.0f;
     if constexpr (SKIP) {
 #pragma unroll
         for (int r = 0; r < 3; ++r) {
             g0[r] = (o[r] - P.bmin[r]) * P.scale[r];
-            ds[r] = d[r] * P.scale[r];
-            inv_ds[r] = __builtin_amdgcn_rcpf(ds[r]);
+            const float ds = d[r] * P.scale[r];
+            inv_ds[r] = ds == 0.0f ? INFINITY : __builtin_amdgcn_rcpf(ds);
         }
         // binary32 rounding of g along the exact path, of g + 1/2 at the node
         // boundary and of this affine estimate all stay below 2^-20 times
@@ -775,7 +774,7 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
         float mag = static_cast<float>(n_p);
 #pragma unroll
         for (int r = 0; r < 3; ++r)
-            mag = fmaxf(mag, fabsf(g0[r]) + fabsf(ds[r]) * fabsf(P.far_t)
+            mag = fmaxf(mag, fabsf(g0[r]) + fabsf(d[r] * P.scale[r]) * fabsf(P.far_t)
                                  + P.scale[r] * (fabsf(P.bmin[r]) + fabsf(P.bmax[r])));
         leap_margin = P.leap_margin + 0x1p-20f * mag;
     }
@@ -808,12 +807,13 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
         const bool inside = in_range & (p[0] >= P.bmin[0]) & (p[0] <= P.bmax[0]) & (p[1] >= P.bmin[1])
                             & (p[1] <= P.bmax[1]) & (p[2] >= P.bmin[2]) & (p[2] <= P.bmax[2]);
         float sigma = 0.0f;
-        uint32_t ix = 0, iy = 0, iz = 0;
+        // node indices are clamped to the grid for any position; they are
+        // used only for samples inside the box
+        const uint32_t ix = nearest_node(p[0], P.bmin[0], P.scale[0], hi_node);
+        const uint32_t iy = nearest_node(p[1], P.bmin[1], P.scale[1], hi_node);
+        const uint32_t iz = nearest_node(p[2], P.bmin[2], P.scale[2], hi_node);
         int32_t leap = 0;
         if (inside) {
-            ix = nearest_node(p[0], P.bmin[0], P.scale[0], hi_node);
-            iy = nearest_node(p[1], P.bmin[1], P.scale[1], hi_node);
-            iz = nearest_node(p[2], P.bmin[2], P.scale[2], hi_node);
             // Eq. 5: a sample in an empty cell of the 3-D cell grid has
             // sigma = 0 without reading the planes
             bool dead = false;
@@ -822,7 +822,7 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
                 const uint32_t cd = P.cell_dist[(cc[0] * P.cell_m + cc[1]) * P.cell_m + cc[2]];
                 if (cd != 0) {
                     dead = true;
-                    leap = leap_cells(P, cd, cc, g0, inv_ds, ds, leap_margin, i);
+                    leap = leap_cells(P, cd, cc, g0, inv_ds, leap_margin, i);
                 }
             }
             if (!dead) {
@@ -848,7 +848,7 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
                     if (dmax != 0) {
                         const int j = (dxy == dmax) ? 0 : ((dyz == dmax) ? 1 : 2);
                         const uint32_t c[3] = {ix, iy, iz};
-                        leap = leap_target(P, j, dmax, c, g0, inv_ds, ds, leap_margin, i);
+                        leap = leap_target(P, j, dmax, c, g0, inv_ds, leap_margin, i);
                     }
                 }
             }
