@@ -1006,12 +1006,15 @@ constexpr int beta_smem_floats()
 
 // Waves per SIMD: the register target, capped by how many 4-wave workgroups
 // the 160 KiB of LDS of a compute unit holds.
-template <typename UT, int DC, bool LIN>
+template <typename UT, int DC, bool LIN, bool NDC = false>
 constexpr int occupancy()
 {
     // the Eq. 5 path holds more per-ray state (LDS row pointers, folded
-    // biases); six waves leave it room without spilling
-    constexpr int rec = waves_per_simd(3 * DC * static_cast<int>(sizeof(UT)));
+    // biases); six waves leave it room without spilling.  The NDC map keeps
+    // a few more values across the march: one wave less (at eight waves the
+    // forward-facing kernel spilled three registers and ran 7% slower).
+    constexpr int rec0 = waves_per_simd(3 * DC * static_cast<int>(sizeof(UT)));
+    constexpr int rec = NDC && rec0 > 4 ? rec0 - 1 : rec0;
     constexpr int regs = LIN && rec > 6 ? 6 : rec;
     constexpr int lds = 4 * (lin_smem_floats<DC, LIN>() + beta_smem_floats<DC, LIN>());
     constexpr int by_lds = 163840 / lds;
@@ -1019,7 +1022,7 @@ constexpr int occupancy()
 }
 
 template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool LIN, bool NDC>
-__global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN>())) void render_kernel(const RenderParams P)
+__global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC>())) void render_kernel(const RenderParams P)
 {
     // beta of every lane's ray, component-major so that a wave-wide read of
     // one component touches consecutive LDS words; each lane reads only what
