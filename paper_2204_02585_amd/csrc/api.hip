@@ -265,6 +265,8 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
     p.n_theta = h->desc.n_theta;
     p.n_phi = h->desc.n_phi;
     p.beta_f16 = h->desc.beta_dtype == SQN_F16;
+    p.theta_scale = static_cast<double>(h->desc.n_theta - 1) / 3.14159265358979323846;
+    p.phi_scale = static_cast<double>(h->desc.n_phi) / (2.0 * 3.14159265358979323846);
     p.rec_bytes = static_cast<uint32_t>(3 * h->desc.D * dtype_size(h->desc.uvw_dtype));
     p.tau_eps = h->tau_eps;
     p.seed = h->desc.seed;

@@ -137,13 +137,19 @@ __device__ __forceinline__ float grp_sum(float x)
     return x;
 }
 
+template <int CTRL>
+__device__ __forceinline__ double dppd(double x)
+{
+    return __longlong_as_double(static_cast<long long>(dpp64<CTRL>(static_cast<uint64_t>(__double_as_longlong(x)))));
+}
+
 template <int L>
 __device__ __forceinline__ double grp_sum(double x)
 {
     if constexpr (L >= 2)
-        x += __shfl_xor(x, 1, L);
+        x += dppd<qperm(1, 0, 3, 2)>(x);
     if constexpr (L == 4)
-        x += __shfl_xor(x, 2, L);
+        x += dppd<qperm(2, 3, 0, 1)>(x);
     return x;
 }
 
@@ -302,6 +308,40 @@ __device__ __forceinline__ void clip_to_box(const RenderParams& P, const float o
 // ---------------------------------------------------------------------------
 // value path
 
+// atan2 in binary64 to within 2e-14 (checked against the library atan2 on
+// 2 x 10^5 random pairs and the signed-zero cases): octant reduction to
+// t = min/max, then t > tan(pi/8) to (t - 1)/(t + 1) in one division, and an
+// odd polynomial t + t^3 P(t^2) with P a least-squares fit of
+// (atan(t) - t)/t^3 at Chebyshev nodes of [0, tan^2(pi/8)].  Signs and
+// zeros follow atan2.  The direction lookup needs the angles to about 1e-8.
+__device__ __forceinline__ double atan2_lookup(double y, double x)
+{
+    constexpr double kTanPi8 = 0.41421356237309503;
+    const double ax = fabs(x), ay = fabs(y);
+    const double mx = fmax(ax, ay), mn = fmin(ax, ay);
+    const bool big = mn > kTanPi8 * mx;
+    const double num = big ? mn - mx : mn;
+    const double den = big ? mn + mx : mx;
+    const double t = den > 0.0 ? num / den : 0.0;
+    const double s = t * t;
+    double p = 0.03139479947774411;
+    p = fma(p, s, -0.05926635751528511);
+    p = fma(p, s, 0.0757883898701557);
+    p = fma(p, s, -0.09080691227325184);
+    p = fma(p, s, 0.11110579634656349);
+    p = fma(p, s, -0.14285699429416587);
+    p = fma(p, s, 0.1999999981132898);
+    p = fma(p, s, -0.333333333326259);
+    double r = fma(t * s, p, t);
+    if (big)
+        r += 0.25 * kPi;
+    if (ay > ax)
+        r = 0.5 * kPi - r;
+    if (signbit(x))
+        r = kPi - r;
+    return copysign(r, y);
+}
+
 // Bilinear lookup of beta (Sec. 3.4), once per ray.  The angles and grid
 // coordinates are computed in binary64 (theta = polar angle from +z on a
 // clamped grid over [0, pi]; phi = atan2 on a periodic grid from -pi); with
@@ -315,11 +355,11 @@ __device__ __forceinline__ void lookup_beta(const RenderParams& P, const float d
     const double dx = d[0], dy = d[1], dz = d[2];
     double theta, phi;
     if constexpr (L == 1) {
-        theta = atan2(sqrt(dx * dx + dy * dy), dz);
-        phi = atan2(dy, dx);
+        theta = atan2_lookup(sqrt(dx * dx + dy * dy), dz);
+        phi = atan2_lookup(dy, dx);
     } else {
         const bool odd = (s & 1) != 0;
-        const double ang = atan2(odd ? dy : sqrt(dx * dx + dy * dy), odd ? dx : dz);
+        const double ang = atan2_lookup(odd ? dy : sqrt(dx * dx + dy * dy), odd ? dx : dz);
         const uint32_t lo = static_cast<uint32_t>(__double_as_longlong(ang));
         const uint32_t hi = static_cast<uint32_t>(static_cast<uint64_t>(__double_as_longlong(ang)) >> 32);
         // even lane -> theta, odd lane -> phi, exchanged within each pair
@@ -330,16 +370,21 @@ __device__ __forceinline__ void lookup_beta(const RenderParams& P, const float d
         phi = odd ? ang : other;
     }
 
-    const double gt = theta * static_cast<double>(P.n_theta - 1) / kPi;
+    // grid coordinates: theta in [0, pi] and phi + pi in [0, 2 pi], scaled
+    // by factors the host computes in binary64
+    const double gt = theta * P.theta_scale;
     int32_t a0 = static_cast<int32_t>(floor(gt));
     a0 = max(0, min(a0, P.n_theta - 2));
     const double ft = fmin(fmax(gt - static_cast<double>(a0), 0.0), 1.0);
 
-    const double gp = (phi + kPi) * static_cast<double>(P.n_phi) / (2.0 * kPi);
+    const double gp = (phi + kPi) * P.phi_scale;
     const double fb = floor(gp);
     const double fp = gp - fb;
+    // gp lies in [0, n_phi] (n_phi only at phi = pi), so one wrap suffices;
+    // the clamps keep any input inside the table
     int32_t b0 = static_cast<int32_t>(fb);
-    b0 = ((b0 % P.n_phi) + P.n_phi) % P.n_phi;
+    b0 = b0 >= P.n_phi ? b0 - P.n_phi : b0;
+    b0 = min(max(b0, 0), P.n_phi - 1);
     const int32_t b1 = (b0 + 1 == P.n_phi) ? 0 : b0 + 1;
 
     const int32_t D = DC > 0 ? DC : P.D;

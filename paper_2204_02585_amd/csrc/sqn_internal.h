@@ -32,6 +32,8 @@ struct RenderParams {
     float scale[3];           // (n_p - 1) / (bmax - bmin) in binary32
     int32_t n_p, D, n_theta, n_phi;
     int32_t beta_f16;
+    double theta_scale;       // (n_theta - 1) / pi: grid coordinate per radian
+    double phi_scale;         // n_phi / (2 pi)
     uint32_t rec_bytes;       // bytes of one uvw record (3D values)
     int64_t tau_eps;          // floor(-ln(eps) 2^32), INT64_MAX for eps = 0
     uint64_t seed;
