@@ -459,12 +459,12 @@ __device__ __forceinline__ float sigmoid(float x)
 
 // Colour of one occupied sample: beta^T (k^xy + k^yz + k^zx) per channel
 // (Eq. 4 and Eq. 2, summed plane by plane), then a sigmoid.
-template <typename UT, int DC>
+template <typename UT, int DC, int BS>
 __device__ __forceinline__ void sample_colour(const RenderParams& P, uint32_t t0, uint32_t t1,
                                               uint32_t t2, const float* beta_lds, float col[3])
 {
-    // beta component k of this lane's ray lives at beta_lds[k * kBlockThreads]
-    auto beta = [&](int k) { return beta_lds[k * kBlockThreads]; };
+    // beta component k of this lane's ray lives at beta_lds[k * BS]
+    auto beta = [&](int k) { return beta_lds[k * BS]; };
     if constexpr (DC > 0 && (3 * DC * sizeof(UT)) % 16 == 0) {
         constexpr int NV = 3 * DC;
         constexpr uint32_t NB = NV * static_cast<uint32_t>(sizeof(UT));
@@ -744,22 +744,21 @@ constexpr int waves_per_simd(int record_bytes)
     return record_bytes == 0 ? 6 : (record_bytes <= 48 ? 8 : (record_bytes <= 96 ? 5 : 4));
 }
 
-// One ray (or, with L lanes per ray, one L-lane group) at pixel (u, v) of
-// view `view`; `lane` is the lane index in the wave.
-// SKIP: leap over runs of samples that one plane's distance field proves
-// empty (with L lanes per ray, the run that starts at the chunk's last
-// sample decides where the next chunk starts).
-template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool LIN, bool NDC>
-__device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, int32_t u,
-                                           int32_t v, int32_t lane, float* const beta, float* const lin)
-{
-    const int32_t s = (L == 1) ? 0 : (lane & (L - 1));
-    const int64_t ray = (static_cast<int64_t>(view) * P.height + v) * P.width + u;
-    const int32_t N = P.n_samples;
-    const bool stratified = P.stratified != 0;
-    const uint64_t ray_key = static_cast<uint64_t>(ray) * static_cast<uint64_t>(N);
+// What the march needs of one ray besides beta: the ray (after the NDC map
+// for forward-facing captures), |d|, the conservative sample range of the
+// box and the affine grid coordinates of the leaps.
+struct RayGeom {
+    float o[3], d[3];
+    float dn;
+    float g0[3], inv_ds[3];   // grid coordinate g = g0 + t ds per axis, 1/ds
+    float margin;             // texels a leap keeps from its square's edge
+    int32_t i0, i1;
+};
 
-    // --- ray through the pixel centre (camera looks down -z) ---
+// World ray through the pixel centre of (u, v) (camera looks down -z).
+__device__ __forceinline__ void pixel_ray(const RenderParams& P, int32_t view, int32_t u, int32_t v,
+                                          float o[3], float d[3])
+{
     const float* pose = P.poses + 12 * static_cast<int64_t>(view);
     float pm[12];
 #pragma unroll
@@ -767,7 +766,6 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
         pm[k] = pose[k];
     const float a = ((static_cast<float>(u) + 0.5f) - P.cx) / P.fx;
     const float b = -(((static_cast<float>(v) + 0.5f) - P.cy) / P.fy);
-    float o[3], d[3];
 #pragma unroll
     for (int r = 0; r < 3; ++r) {
         const float pa = pm[4 * r + 0] * a;
@@ -775,54 +773,109 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
         d[r] = (pa + pb) - pm[4 * r + 2];
         o[r] = pm[4 * r + 3];
     }
-    // direction weights from the world direction
-    if constexpr (LIN) {
-        // beta goes to the ray's LDS row (the L lanes write equal values)
-        lookup_beta<DC, L, 1>(P, d, s, DC > 0 ? lin : lin + 9 * P.D + 3);
-        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-        fold_decoder<DC, L>(P, s, lin);
-    } else {
-        lookup_beta<DC, L, kBlockThreads>(P, d, s, beta);
-    }
+}
 
+// RayGeom from the world ray (o, d): NDC map, |d|, box clip, leap constants.
+template <bool SKIP, bool NDC>
+__device__ __forceinline__ void march_geometry(const RenderParams& P, const float o_w[3], const float d_w[3],
+                                               RayGeom& g)
+{
+#pragma unroll
+    for (int r = 0; r < 3; ++r) {
+        g.o[r] = o_w[r];
+        g.d[r] = d_w[r];
+    }
     // forward-facing captures march in normalized device coordinates
     bool no_samples = false;
     if constexpr (NDC)
-        no_samples = !ndc_ray(P, o, d);
-    const float d00 = d[0] * d[0], d11 = d[1] * d[1], d22 = d[2] * d[2];
-    const float dn = sqrtf((d00 + d11) + d22);
-
-    int32_t i0, i1;
-    clip_to_box(P, o, d, i0, i1);
+        no_samples = !ndc_ray(P, g.o, g.d);
+    const float d00 = g.d[0] * g.d[0], d11 = g.d[1] * g.d[1], d22 = g.d[2] * g.d[2];
+    g.dn = sqrtf((d00 + d11) + d22);
+    clip_to_box(P, g.o, g.d, g.i0, g.i1);
     if constexpr (NDC) {
         if (no_samples) {
-            i0 = 1;
-            i1 = 0;
+            g.i0 = 1;
+            g.i1 = 0;
         }
     }
-
-    const int32_t n_p = P.n_p;
-    const float hi_node = static_cast<float>(n_p - 1);
-    // grid coordinate of each axis as an affine function of t, for leaps
-    float g0[3], inv_ds[3];
-    float leap_margin = 0.0f;
+    g.margin = 0.0f;
     if constexpr (SKIP) {
 #pragma unroll
         for (int r = 0; r < 3; ++r) {
-            g0[r] = (o[r] - P.bmin[r]) * P.scale[r];
-            const float ds = d[r] * P.scale[r];
-            inv_ds[r] = ds == 0.0f ? INFINITY : __builtin_amdgcn_rcpf(ds);
+            g.g0[r] = (g.o[r] - P.bmin[r]) * P.scale[r];
+            const float ds = g.d[r] * P.scale[r];
+            g.inv_ds[r] = ds == 0.0f ? INFINITY : __builtin_amdgcn_rcpf(ds);
         }
         // binary32 rounding of g along the exact path, of g + 1/2 at the node
         // boundary and of this affine estimate all stay below 2^-20 times
         // the magnitudes involved (about 16 units in the last place)
-        float mag = static_cast<float>(n_p);
+        float mag = static_cast<float>(P.n_p);
 #pragma unroll
         for (int r = 0; r < 3; ++r)
-            mag = fmaxf(mag, fabsf(g0[r]) + fabsf(d[r] * P.scale[r]) * fabsf(P.far_t)
+            mag = fmaxf(mag, fabsf(g.g0[r]) + fabsf(g.d[r] * P.scale[r]) * fabsf(P.far_t)
                                  + P.scale[r] * (fabsf(P.bmin[r]) + fabsf(P.bmax[r])));
-        leap_margin = P.leap_margin + 0x1p-20f * mag;
+        g.margin = P.leap_margin + 0x1p-20f * mag;
     }
+}
+
+// One ray (or, with L lanes per ray, one L-lane group) at pixel (u, v) of
+// view `view`; `lane` is the lane index in the wave.
+// SKIP: leap over runs of samples that one plane's distance field proves
+// empty (with L lanes per ray, the run that starts at the chunk's last
+// sample decides where the next chunk starts).
+// COOP: the workgroup computed the ray's geometry and beta once per ray
+// (`pre`; beta at beta[k * BS]) instead of in each of its L lanes.
+template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool LIN, bool NDC, bool COOP = false,
+          int BS = kBlockThreads>
+__device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, int32_t u,
+                                           int32_t v, int32_t lane, float* const beta, float* const lin,
+                                           const RayGeom* pre = nullptr)
+{
+    const int32_t s = (L == 1) ? 0 : (lane & (L - 1));
+    const int64_t ray = (static_cast<int64_t>(view) * P.height + v) * P.width + u;
+    const int32_t N = P.n_samples;
+    const bool stratified = P.stratified != 0;
+    const uint64_t ray_key = static_cast<uint64_t>(ray) * static_cast<uint64_t>(N);
+
+    RayGeom geo;
+    if constexpr (COOP) {
+        geo = *pre;
+        if constexpr (!NDC) {
+            // a world ray starts at the camera centre, the same for the whole
+            // view: taken from the pose, it and its grid coordinates stay in
+            // scalar registers (the same binary32 operations as the setup)
+            const float* pose = P.poses + 12 * static_cast<int64_t>(view);
+#pragma unroll
+            for (int r = 0; r < 3; ++r) {
+                geo.o[r] = pose[4 * r + 3];
+                if constexpr (SKIP)
+                    geo.g0[r] = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(
+                                    int, (geo.o[r] - P.bmin[r]) * P.scale[r])));
+            }
+        }
+    } else {
+        float o_w[3], d_w[3];
+        pixel_ray(P, view, u, v, o_w, d_w);
+        // direction weights from the world direction
+        if constexpr (LIN) {
+            // beta goes to the ray's LDS row (the L lanes write equal values)
+            lookup_beta<DC, L, 1>(P, d_w, s, DC > 0 ? lin : lin + 9 * P.D + 3);
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+            fold_decoder<DC, L>(P, s, lin);
+        } else {
+            lookup_beta<DC, L, BS>(P, d_w, s, beta);
+        }
+        march_geometry<SKIP, NDC>(P, o_w, d_w, geo);
+    }
+    const float* const o = geo.o;
+    const float* const d = geo.d;
+    const float dn = geo.dn;
+    const int32_t i0 = geo.i0, i1 = geo.i1;
+    const float* const g0 = geo.g0;
+    const float* const inv_ds = geo.inv_ds;
+    const float leap_margin = geo.margin;
+    const int32_t n_p = P.n_p;
+    const float hi_node = static_cast<float>(n_p - 1);
     uint64_t tau = 0;              // optical depth before the chunk, 2^-32 units
     double acc_r = 0.0, acc_g = 0.0, acc_b = 0.0, acc_t = 0.0;
     int32_t last_live = -1;
@@ -946,8 +999,8 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
                 sample_colour_lin<UT, DC>(P, __umul24(ix, n_p) + iy, __umul24(iy, n_p) + iz,
                                           __umul24(iz, n_p) + ix, lin, col);
             else
-                sample_colour<UT, DC>(P, __umul24(ix, n_p) + iy, __umul24(iy, n_p) + iz,
-                                      __umul24(iz, n_p) + ix, beta, col);
+                sample_colour<UT, DC, BS>(P, __umul24(ix, n_p) + iy, __umul24(iy, n_p) + iz,
+                                          __umul24(iz, n_p) + ix, beta, col);
             const float T = transmittance(tau_i);
             const float alpha = -expm1f(-q);
             const double w = static_cast<double>(T * alpha);
@@ -1041,25 +1094,27 @@ constexpr int lin_smem_floats()
     return LIN ? (DC > 0 ? lin_stride(DC) : lin_stride_generic(32)) * (kBlockThreads / 4) : 4;
 }
 
-// LDS floats of beta per workgroup (one copy per lane; Eq. 5 keeps it in
-// the folded rows instead).
-template <int DC, bool LIN>
+// LDS floats of beta per workgroup: one copy per lane with one lane per
+// ray, one per ray (64) with four; Eq. 5 keeps it in the folded rows.
+template <int DC, bool LIN, int L = 1>
 constexpr int beta_smem_floats()
 {
-    return LIN ? 4 : (DC > 0 ? DC : 32) * kBlockThreads;
+    return LIN ? 4 : (DC > 0 ? DC : 32) * (L == 4 ? 64 : kBlockThreads);
 }
 
 // Waves per SIMD: the register target, capped by how many 4-wave workgroups
 // the 160 KiB of LDS of a compute unit holds.
-template <typename UT, int DC, bool LIN, bool NDC = false>
+template <typename UT, int DC, bool LIN, bool NDC = false, int L = 1>
 constexpr int occupancy()
 {
     // the Eq. 5 path holds more per-ray state (LDS row pointers, folded
     // biases); six waves leave it room without spilling.  The NDC map keeps
-    // a few more values across the march: one wave less (at eight waves the
-    // forward-facing kernel spilled three registers and ran 7% slower).
+    // a few more values across the march (at eight waves the forward-facing
+    // kernel spilled three registers and ran 7% slower), and the four-lane
+    // kernels that read their ray setup from LDS measured 3-4% faster at
+    // seven waves than at eight: one wave less for both.
     constexpr int rec0 = waves_per_simd(3 * DC * static_cast<int>(sizeof(UT)));
-    constexpr int rec = NDC && rec0 > 4 ? rec0 - 1 : rec0;
+    constexpr int rec = (NDC || (L == 4 && !LIN)) && rec0 > 4 ? rec0 - 1 : rec0;
     constexpr int regs = LIN && rec > 6 ? 6 : rec;
     constexpr int lds = 4 * (lin_smem_floats<DC, LIN>() + beta_smem_floats<DC, LIN>());
     constexpr int by_lds = 163840 / lds;
@@ -1067,12 +1122,12 @@ constexpr int occupancy()
 }
 
 template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool LIN, bool NDC>
-__global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC>())) void render_kernel(const RenderParams P)
+__global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) void render_kernel(const RenderParams P)
 {
     // beta of every lane's ray, component-major so that a wave-wide read of
     // one component touches consecutive LDS words; each lane reads only what
     // it wrote, so no barrier is needed
-    __shared__ float beta_smem[beta_smem_floats<DC, LIN>()];
+    __shared__ float beta_smem[beta_smem_floats<DC, LIN, L>()];
     // Eq. 5: one row of folded weights per ray, written and read only by
     // the ray's own lanes
     __shared__ __align__(16) float lin_smem[lin_smem_floats<DC, LIN>()];
@@ -1087,15 +1142,43 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC>())) voi
     const int32_t slot = lane / L;
     const int32_t u = tx * kTileW(L) + (wave & 1) * WW + (slot % WW);
     const int32_t v = ty * kTileH(L) + (wave >> 1) * WH + (slot / WW);
-    // all lanes of a ray agree on this, so a lane group is never split
-    if (view < P.n_views && u < P.width && v < P.height) {
-        float* lin = nullptr;
-        if constexpr (LIN) {
-            constexpr int32_t stride = DC > 0 ? lin_stride(DC) : 0;
-            lin = lin_smem + (threadIdx.x / 4) * (DC > 0 ? stride : P.lin_stride);
+    if constexpr (L == 4 && !LIN) {
+        // Four lanes per ray: the first wave computes beta and the second
+        // the march geometry of the workgroup's 64 rays, one lane per ray,
+        // and the four waves march from them; the ray setup then costs one
+        // wave's instructions per workgroup instead of four (the march is
+        // bound by vector-ALU issue).
+        __shared__ RayGeom geom[64];
+        if (wave < 2) {
+            const int32_t w = lane >> 4, sl = lane & 15;
+            const int32_t ur = tx * kTileW(L) + (w & 1) * WW + (sl % WW);
+            const int32_t vr = ty * kTileH(L) + (w >> 1) * WH + (sl / WW);
+            if (view < P.n_views && ur < P.width && vr < P.height) {
+                float o_w[3], d_w[3];
+                pixel_ray(P, view, ur, vr, o_w, d_w);
+                // wave 0: beta, wave 1: the march geometry
+                if (wave == 0)
+                    lookup_beta<DC, 1, 64>(P, d_w, 0, beta_smem + lane);
+                else
+                    march_geometry<SKIP, NDC>(P, o_w, d_w, geom[lane]);
+            }
         }
-        render_ray<ST, UT, DC, STATS, L, SKIP, LIN, NDC>(P, view, u, v, lane,
-                                                    LIN ? beta_smem : beta_smem + threadIdx.x, lin);
+        __syncthreads();
+        const int32_t r = wave * 16 + slot;
+        if (view < P.n_views && u < P.width && v < P.height)
+            render_ray<ST, UT, DC, STATS, L, SKIP, LIN, NDC, true, 64>(P, view, u, v, lane, beta_smem + r, nullptr,
+                                                                      &geom[r]);
+    } else {
+        // all lanes of a ray agree on this, so a lane group is never split
+        if (view < P.n_views && u < P.width && v < P.height) {
+            float* lin = nullptr;
+            if constexpr (LIN) {
+                constexpr int32_t stride = DC > 0 ? lin_stride(DC) : 0;
+                lin = lin_smem + (threadIdx.x / 4) * (DC > 0 ? stride : P.lin_stride);
+            }
+            render_ray<ST, UT, DC, STATS, L, SKIP, LIN, NDC>(P, view, u, v, lane,
+                                                        LIN ? beta_smem : beta_smem + threadIdx.x, lin);
+        }
     }
 }
 
