@@ -840,6 +840,9 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
     RayGeom geo;
     if constexpr (COOP) {
         geo = *pre;
+        // Eq. 5: beta waits in the ray's LDS row; the L lanes fold it
+        if constexpr (LIN)
+            fold_decoder<DC, L>(P, s, lin);
         if constexpr (!NDC) {
             // a world ray starts at the camera centre, the same for the whole
             // view: taken from the pose, it and its grid coordinates stay in
@@ -1142,13 +1145,16 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) 
     const int32_t slot = lane / L;
     const int32_t u = tx * kTileW(L) + (wave & 1) * WW + (slot % WW);
     const int32_t v = ty * kTileH(L) + (wave >> 1) * WH + (slot / WW);
-    if constexpr (L == 4 && !LIN) {
+    if constexpr (L == 4) {
         // Four lanes per ray: the first wave computes beta and the second
         // the march geometry of the workgroup's 64 rays, one lane per ray,
         // and the four waves march from them; the ray setup then costs one
         // wave's instructions per workgroup instead of four (the march is
-        // bound by vector-ALU issue).
+        // bound by vector-ALU issue).  Eq. 5 keeps beta in the ray's row of
+        // folded weights, which the ray's four lanes then fold.
         __shared__ RayGeom geom[64];
+        constexpr int32_t stride = LIN && DC > 0 ? lin_stride(DC) : 0;
+        auto lin_row = [&](int32_t r) { return lin_smem + r * (DC > 0 ? stride : P.lin_stride); };
         if (wave < 2) {
             const int32_t w = lane >> 4, sl = lane & 15;
             const int32_t ur = tx * kTileW(L) + (w & 1) * WW + (sl % WW);
@@ -1157,17 +1163,21 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) 
                 float o_w[3], d_w[3];
                 pixel_ray(P, view, ur, vr, o_w, d_w);
                 // wave 0: beta, wave 1: the march geometry
-                if (wave == 0)
-                    lookup_beta<DC, 1, 64>(P, d_w, 0, beta_smem + lane);
-                else
+                if (wave == 0) {
+                    if constexpr (LIN)
+                        lookup_beta<DC, 1, 1>(P, d_w, 0, DC > 0 ? lin_row(lane) : lin_row(lane) + 9 * P.D + 3);
+                    else
+                        lookup_beta<DC, 1, 64>(P, d_w, 0, beta_smem + lane);
+                } else {
                     march_geometry<SKIP, NDC>(P, o_w, d_w, geom[lane]);
+                }
             }
         }
         __syncthreads();
         const int32_t r = wave * 16 + slot;
         if (view < P.n_views && u < P.width && v < P.height)
-            render_ray<ST, UT, DC, STATS, L, SKIP, LIN, NDC, true, 64>(P, view, u, v, lane, beta_smem + r, nullptr,
-                                                                      &geom[r]);
+            render_ray<ST, UT, DC, STATS, L, SKIP, LIN, NDC, true, 64>(P, view, u, v, lane, beta_smem + r,
+                                                                      LIN ? lin_row(r) : nullptr, &geom[r]);
     } else {
         // all lanes of a ray agree on this, so a lane group is never split
         if (view < P.n_views && u < P.width && v < P.height) {
