@@ -243,7 +243,7 @@ def main():
     ap.add_argument("--config", default="paper", choices=sorted(WORKLOAD_TEXT) + sorted(GEN_TEXT),
                     help="a render workload, or gen_* for cache generation")
     ap.add_argument("--lanes", type=int, default=0,
-                    help="lanes of a wavefront per ray (1 or 4); 0 = the library's choice")
+                    help="lanes of a wavefront per ray (1, 4 or 8); 0 = the library's choice")
     ap.add_argument("--dense", action="store_true",
                     help="march every sample (no leaps over empty space)")
     ap.add_argument("--no-cpu-baseline", action="store_true")

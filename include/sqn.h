@@ -192,13 +192,14 @@ sqn_status sqn_render_stats(const sqn_caches* caches,
                             void* stream);
 
 /* Launch shape of later renders with this handle: how many lanes of a
- * wavefront share one ray (1 or 4; the L lanes take the L consecutive
+ * wavefront share one ray (1, 4 or 8; the L lanes take the L consecutive
  * samples of a chunk), or 0 (the default) to choose per call from the number
- * of rays.  Sample, index and termination decisions are identical for every
- * choice; colour and depth agree up to the rounding of their sums.  Not
- * thread-safe against concurrent renders with the handle.
- * Errors: SQN_ERR_INVALID_ARG; SQN_ERR_UNSUPPORTED for 1 on a handle made
- * by sqn_create_linear_caches (always four lanes). */
+ * of rays (8 below 2^18 rays, 4 below 2^20, else 1).  Sample, index and
+ * termination decisions are identical for every choice; colour and depth
+ * agree up to the rounding of their sums.  Not thread-safe against
+ * concurrent renders with the handle.
+ * Errors: SQN_ERR_INVALID_ARG; SQN_ERR_UNSUPPORTED for 1 or 8 on a handle
+ * made by sqn_create_linear_caches (always four lanes). */
 sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes);
 
 /* Leaps over empty space (1, the default) or a dense march (0).  sigma is

@@ -204,7 +204,7 @@ class Caches:
         return int(lib.sqn_cache_device_bytes(self.handle))
 
     def set_lanes_per_ray(self, lanes: int) -> None:
-        """1 or 4 lanes of a wavefront per ray, or 0 to choose per call."""
+        """1, 4 or 8 lanes of a wavefront per ray, or 0 to choose per call."""
         _check(lib.sqn_set_lanes_per_ray(self.handle, int(lanes)))
 
     def set_empty_space_skipping(self, enable: bool) -> None:

@@ -44,10 +44,13 @@ __device__ __forceinline__ T load_at(const void* base, uint32_t off)
 }
 
 // ---------------------------------------------------------------------------
-// lanes of one ray: L consecutive lanes inside a quad, exchanged with DPP
-// quad permutations (the group is always entirely active or inactive)
+// lanes of one ray: L = 2 or 4 consecutive lanes inside a quad, exchanged
+// with DPP quad permutations, or L = 8 lanes of a half-row, whose two quads
+// also exchange through the half-row mirror (lane i <-> 7 - i); the group is
+// always entirely active or inactive
 
 constexpr int qperm(int a, int b, int c, int d) { return a | (b << 2) | (c << 4) | (d << 6); }
+constexpr int kHalfMirror = 0x141;   // DPP row_half_mirror
 
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp32(uint32_t x)
@@ -77,7 +80,12 @@ __device__ __forceinline__ float grp_next(float x)
         return dppf<qperm(1, 1, 3, 3)>(x);
     else if constexpr (L == 4)
         return dppf<qperm(1, 2, 3, 3)>(x);
-    else
+    else if constexpr (L == 8) {
+        // lane 3 takes lane 4 from the other quad (7 - 3 = 4)
+        const float a = dppf<qperm(1, 2, 3, 3)>(x);
+        const float b = dppf<kHalfMirror>(x);
+        return ((__lane_id() & 7) == 3) ? b : a;
+    } else
         return x;
 }
 
@@ -89,7 +97,12 @@ __device__ __forceinline__ float grp_first(float x)
         return dppf<qperm(0, 0, 2, 2)>(x);
     else if constexpr (L == 4)
         return dppf<qperm(0, 0, 0, 0)>(x);
-    else
+    else if constexpr (L == 8) {
+        // the upper quad reads lane 0 where the mirror put it, in lane 7
+        const float a = dppf<qperm(0, 0, 0, 0)>(x);
+        const float b = dppf<qperm(3, 3, 3, 3)>(dppf<kHalfMirror>(x));
+        return ((__lane_id() & 7) < 4) ? a : b;
+    } else
         return x;
 }
 
@@ -117,13 +130,23 @@ __device__ __forceinline__ void grp_scan(uint64_t q, int s, uint64_t& excl, uint
         excl = s ? other : 0;
         total = q + other;
     } else {
+        const int sq = s & 3;
         uint64_t y = q;
         const uint64_t y1 = dpp64<qperm(0, 0, 1, 2)>(y);
-        y += (s >= 1) ? y1 : 0;
+        y += (sq >= 1) ? y1 : 0;
         const uint64_t y2 = dpp64<qperm(0, 0, 0, 1)>(y);
-        y += (s >= 2) ? y2 : 0;
-        excl = y - q;
-        total = dpp64<qperm(3, 3, 3, 3)>(y);
+        y += (sq >= 2) ? y2 : 0;
+        const uint64_t tq = dpp64<qperm(3, 3, 3, 3)>(y);
+        if constexpr (L == 8) {
+            // the other quad's total; the upper quad adds the lower one's
+            const uint64_t other = dpp64<kHalfMirror>(tq);
+            y += (s >= 4) ? other : 0;
+            excl = y - q;
+            total = tq + other;
+        } else {
+            excl = y - q;
+            total = tq;
+        }
     }
 }
 
@@ -132,8 +155,10 @@ __device__ __forceinline__ float grp_sum(float x)
 {
     if constexpr (L >= 2)
         x += dppf<qperm(1, 0, 3, 2)>(x);
-    if constexpr (L == 4)
+    if constexpr (L >= 4)
         x += dppf<qperm(2, 3, 0, 1)>(x);
+    if constexpr (L == 8)
+        x += dppf<kHalfMirror>(x);
     return x;
 }
 
@@ -148,8 +173,10 @@ __device__ __forceinline__ double grp_sum(double x)
 {
     if constexpr (L >= 2)
         x += dppd<qperm(1, 0, 3, 2)>(x);
-    if constexpr (L == 4)
+    if constexpr (L >= 4)
         x += dppd<qperm(2, 3, 0, 1)>(x);
+    if constexpr (L == 8)
+        x += dppd<kHalfMirror>(x);
     return x;
 }
 
@@ -158,8 +185,10 @@ __device__ __forceinline__ int32_t grp_max(int32_t x)
 {
     if constexpr (L >= 2)
         x = max(x, static_cast<int32_t>(dpp32<qperm(1, 0, 3, 2)>(static_cast<uint32_t>(x))));
-    if constexpr (L == 4)
+    if constexpr (L >= 4)
         x = max(x, static_cast<int32_t>(dpp32<qperm(2, 3, 0, 1)>(static_cast<uint32_t>(x))));
+    if constexpr (L == 8)
+        x = max(x, static_cast<int32_t>(dpp32<kHalfMirror>(static_cast<uint32_t>(x))));
     return x;
 }
 
@@ -168,8 +197,10 @@ __device__ __forceinline__ uint32_t grp_add(uint32_t x)
 {
     if constexpr (L >= 2)
         x += dpp32<qperm(1, 0, 3, 2)>(x);
-    if constexpr (L == 4)
+    if constexpr (L >= 4)
         x += dpp32<qperm(2, 3, 0, 1)>(x);
+    if constexpr (L == 8)
+        x += dpp32<kHalfMirror>(x);
     return x;
 }
 
@@ -821,8 +852,8 @@ __device__ __forceinline__ void march_geometry(const RenderParams& P, const floa
 // One ray (or, with L lanes per ray, one L-lane group) at pixel (u, v) of
 // view `view`; `lane` is the lane index in the wave.
 // SKIP: leap over runs of samples that one plane's distance field proves
-// empty (with L lanes per ray, the run that starts at the chunk's last
-// sample decides where the next chunk starts).
+// empty (with L lanes per ray, the next chunk starts at the furthest end of
+// the runs its lanes found).
 // COOP: the workgroup computed the ray's geometry and beta once per ray
 // (`pre`; beta at beta[k * BS]) instead of in each of its L lanes.
 template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool LIN, bool NDC, bool COOP = false,
@@ -1087,7 +1118,7 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
     }
 }
 
-// Launch shapes: L = 1 or 4 lanes per ray over workgroup tiles of
+// Launch shapes: L = 1, 4 or 8 lanes per ray over workgroup tiles of
 // kTileW(L) x kTileH(L) pixels, with or without leaps over empty space.
 // LDS floats of the folded Eq. 5 weights per workgroup (64 rays); a run-time
 // D also keeps beta after the rows.
@@ -1114,10 +1145,11 @@ constexpr int occupancy()
     // biases); six waves leave it room without spilling.  The NDC map keeps
     // a few more values across the march (at eight waves the forward-facing
     // kernel spilled three registers and ran 7% slower), and the four-lane
-    // kernels that read their ray setup from LDS measured 3-4% faster at
-    // seven waves than at eight: one wave less for both.
+    // kernels that read their ray setup from LDS (four or eight lanes)
+    // measured 3-4% faster at seven waves than at eight: one wave less for
+    // both.
     constexpr int rec0 = waves_per_simd(3 * DC * static_cast<int>(sizeof(UT)));
-    constexpr int rec = (NDC || (L == 4 && !LIN)) && rec0 > 4 ? rec0 - 1 : rec0;
+    constexpr int rec = (NDC || (L >= 4 && !LIN)) && rec0 > 4 ? rec0 - 1 : rec0;
     constexpr int regs = LIN && rec > 6 ? 6 : rec;
     constexpr int lds = 4 * (lin_smem_floats<DC, LIN>() + beta_smem_floats<DC, LIN>());
     constexpr int by_lds = 163840 / lds;
@@ -1145,18 +1177,19 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) 
     const int32_t slot = lane / L;
     const int32_t u = tx * kTileW(L) + (wave & 1) * WW + (slot % WW);
     const int32_t v = ty * kTileH(L) + (wave >> 1) * WH + (slot / WW);
-    if constexpr (L == 4) {
-        // Four lanes per ray: the first wave computes beta and the second
-        // the march geometry of the workgroup's 64 rays, one lane per ray,
-        // and the four waves march from them; the ray setup then costs one
-        // wave's instructions per workgroup instead of four (the march is
-        // bound by vector-ALU issue).  Eq. 5 keeps beta in the ray's row of
-        // folded weights, which the ray's four lanes then fold.
+    if constexpr (L >= 4) {
+        // Four or eight lanes per ray: the first wave computes beta and the
+        // second the march geometry of the workgroup's 256 / L rays, one lane
+        // per ray, and the four waves march from them; the ray setup then
+        // costs one wave's instructions per workgroup instead of L (the
+        // march is bound by vector-ALU issue).  Eq. 5 (four lanes) keeps
+        // beta in the ray's row of folded weights, which its lanes fold.
         __shared__ RayGeom geom[64];
         constexpr int32_t stride = LIN && DC > 0 ? lin_stride(DC) : 0;
         auto lin_row = [&](int32_t r) { return lin_smem + r * (DC > 0 ? stride : P.lin_stride); };
-        if (wave < 2) {
-            const int32_t w = lane >> 4, sl = lane & 15;
+        constexpr int32_t RPW = 64 / L;   // rays per wave
+        if (wave < 2 && lane < 4 * RPW) {
+            const int32_t w = lane / RPW, sl = lane % RPW;
             const int32_t ur = tx * kTileW(L) + (w & 1) * WW + (sl % WW);
             const int32_t vr = ty * kTileH(L) + (w >> 1) * WH + (sl / WW);
             if (view < P.n_views && ur < P.width && vr < P.height) {
@@ -1174,7 +1207,7 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) 
             }
         }
         __syncthreads();
-        const int32_t r = wave * 16 + slot;
+        const int32_t r = wave * RPW + slot;
         if (view < P.n_views && u < P.width && v < P.height)
             render_ray<ST, UT, DC, STATS, L, SKIP, LIN, NDC, true, 64>(P, view, u, v, lane, beta_smem + r,
                                                                       LIN ? lin_row(r) : nullptr, &geom[r]);
@@ -1218,6 +1251,9 @@ hipError_t launch_typed(const RenderParams& p, bool stats, hipStream_t stream)
     if (p.lanes == 1)
         return p.skip ? launch_shape<ST, UT, DC, 1, true, false>(p, stats, stream)
                       : launch_shape<ST, UT, DC, 1, false, false>(p, stats, stream);
+    if (p.lanes == 8)
+        return p.skip ? launch_shape<ST, UT, DC, 8, true, false>(p, stats, stream)
+                      : launch_shape<ST, UT, DC, 8, false, false>(p, stats, stream);
     return p.skip ? launch_shape<ST, UT, DC, 4, true, false>(p, stats, stream)
                   : launch_shape<ST, UT, DC, 4, false, false>(p, stats, stream);
 }

@@ -157,10 +157,10 @@ struct GenParams {
 hipError_t launch_generate(const GenParams& p, _Float16* enc_table, hipStream_t stream);
 
 // Workgroup geometry: 256 threads = 4 wave64; with L lanes per ray a wave
-// holds 64/L rays laid out as a wave tile of kWaveW(L) x kWaveH(L) pixels and
-// a workgroup covers 2 x 2 wave tiles.
+// holds 64/L rays laid out as a wave tile of kWaveW(L) x kWaveH(L) pixels
+// (8x8, 4x4 or 4x2 for L = 1, 4, 8) and a workgroup covers 2 x 2 wave tiles.
 constexpr int kBlockThreads = 256;
-constexpr int kWaveW(int L) { return L == 4 ? 4 : 8; }
+constexpr int kWaveW(int L) { return L >= 4 ? 4 : 8; }
 constexpr int kWaveH(int L) { return (64 / L) / kWaveW(L); }
 constexpr int kTileW(int L) { return 2 * kWaveW(L); }
 constexpr int kTileH(int L) { return 2 * kWaveH(L); }

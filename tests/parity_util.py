@@ -12,8 +12,9 @@ def scene_atol(scene):
 
 
 # launch variants: library default (leaps, lanes chosen per call), leaps with
-# 1 or 4 lanes per ray, and the dense march with 1 or 4 lanes per ray
-MODES = {"auto": (0, True), "skip1": (1, True), "skip4": (4, True), "L1": (1, False), "L4": (4, False)}
+# 1, 4 or 8 lanes per ray, and the dense march with 1, 4 or 8 lanes per ray
+MODES = {"auto": (0, True), "skip1": (1, True), "skip4": (4, True), "skip8": (8, True),
+         "L1": (1, False), "L4": (4, False), "L8": (8, False)}
 
 
 def gpu_render(scene, t_eps=None, poses=None, n_samples=None, stats=True, mode="auto"):

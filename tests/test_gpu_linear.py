@@ -195,9 +195,10 @@ def test_linear_handle_options():
     sc = scenes.make_scene("tiny_alt")
     caches = binding.caches_from_scene(sc)
     try:
-        with pytest.raises(binding.SqnError) as e:
-            caches.set_lanes_per_ray(1)
-        assert e.value.status == binding.SQN_ERR_UNSUPPORTED
+        for other in (1, 8):
+            with pytest.raises(binding.SqnError) as e:
+                caches.set_lanes_per_ray(other)
+            assert e.value.status == binding.SQN_ERR_UNSUPPORTED
         caches.set_lanes_per_ray(4)
         caches.set_lanes_per_ray(0)
         caches.set_empty_space_skipping(False)

@@ -296,10 +296,10 @@ def test_launch_option_validation():
     sc = scenes.make_scene("tiny")
     caches = binding.caches_from_scene(sc)
     try:
-        for bad in (2, 3, -1, 8):
+        for bad in (2, 3, -1, 16):
             with pytest.raises(binding.SqnError):
                 caches.set_lanes_per_ray(bad)
-        for good in (0, 1, 4):
+        for good in (0, 1, 4, 8):
             caches.set_lanes_per_ray(good)
         for bad in (2, -1):
             assert binding.lib.sqn_set_empty_space_skipping(caches.handle, bad) == binding.SQN_ERR_INVALID_ARG
