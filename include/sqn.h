@@ -112,6 +112,8 @@ typedef struct {
  * sqn_destroy); on failure *out is NULL and nothing is leaked.
  * Errors: SQN_ERR_INVALID_ARG (NULL pointer, range, a pointer that is not
  * HIP device memory or whose allocation is smaller than the array),
+ * SQN_ERR_UNSUPPORTED (a uvw plane or the direction cache of 2^32 bytes or
+ * more: the kernels address them with 32-bit offsets),
  * SQN_ERR_OUT_OF_MEMORY, SQN_ERR_DEVICE. */
 sqn_status sqn_create_caches(const sqn_cache_desc* desc,
                              const void* const sigma_planes[3],

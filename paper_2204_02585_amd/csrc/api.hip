@@ -130,6 +130,11 @@ sqn_status validate_desc(const sqn_cache_desc* d)
     if (uvw_plane >= (uint64_t{1} << 32))
         return fail(SQN_ERR_UNSUPPORTED, "a uvw plane of %llu bytes exceeds 2^32 bytes",
                     static_cast<unsigned long long>(uvw_plane));
+    // so is the direction cache
+    const uint64_t beta_bytes = static_cast<uint64_t>(d->n_theta) * d->n_phi * d->D * dtype_size(d->beta_dtype);
+    if (beta_bytes >= (uint64_t{1} << 32))
+        return fail(SQN_ERR_UNSUPPORTED, "a direction cache of %llu bytes exceeds 2^32 bytes",
+                    static_cast<unsigned long long>(beta_bytes));
     return SQN_OK;
 }
 

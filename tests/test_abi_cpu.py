@@ -73,6 +73,13 @@ def test_validation_before_device_calls(lib):
     desc.n_p, desc.D = 8192, 32
     assert lib.lib.sqn_create_caches(ctypes.byref(desc), planes, planes, None, None,
                                      ctypes.byref(out)) == lib.SQN_ERR_UNSUPPORTED
+    # a direction cache the 32-bit offsets cannot address (2^31 binary32 values)
+    desc.n_p, desc.D = 64, 8
+    desc.n_theta, desc.n_phi = 65536, 4096
+    assert lib.lib.sqn_create_caches(ctypes.byref(desc), planes, planes, None, None,
+                                     ctypes.byref(out)) == lib.SQN_ERR_UNSUPPORTED
+    assert "direction cache" in lib.last_error()
+    desc.n_theta, desc.n_phi = 4, 4
     intr = lib.Intrinsics(1.0, 1.0, 0.5, 0.5, 1, 1)
     assert lib.lib.sqn_render(None, None, 1, ctypes.byref(intr), 2.0, 6.0, 8, None, None,
                               None) == lib.SQN_ERR_INVALID_ARG
