@@ -1,13 +1,14 @@
 // Render kernels of the cached SqueezeNeRF path for gfx950 (CDNA4).
 //
-// Work layout.  L consecutive lanes of a wave64 (L = 1, 2 or 4) share one
+// Work layout.  L consecutive lanes of a wave64 (L = 1, 4 or 8) share one
 // pixel ray and walk its samples in chunks of L consecutive samples, one per
 // lane; a wave holds 64/L rays laid out as a compact pixel tile.  Rays of a
 // tile sit a fraction of a texel apart at equal sample index (samples lie on
 // equal-depth planes), so the nearest-node gathers of one wave-wide load hit
 // a few texels and cache lines.  L > 1 multiplies the number of waves of a
 // frame (a single 800x800 view is only 10^4 waves at L = 1) at the price of a
-// short cross-lane scan per chunk.
+// short cross-lane scan per chunk; the per-ray setup is then computed once
+// per ray by the workgroup, not by each of its L lanes.
 //
 // Per ray: pinhole ray (Sec. 3.1); a conservative clip of the sample range to
 // the scene box (samples outside it have sigma = 0 and add nothing); the
@@ -373,33 +374,16 @@ __device__ __forceinline__ double atan2_lookup(double y, double x)
     return copysign(r, y);
 }
 
-// Bilinear lookup of beta (Sec. 3.4), once per ray.  The angles and grid
-// coordinates are computed in binary64 (theta = polar angle from +z on a
-// clamped grid over [0, pi]; phi = atan2 on a periodic grid from -pi); with
-// L >= 2 the even lanes of the group evaluate theta and the odd lanes phi,
-// and each lane weights a share of the four corner texels before a group
-// sum.
-template <int DC, int L, int BS>
-__device__ __forceinline__ void lookup_beta(const RenderParams& P, const float d[3], int s,
-                                            float* beta_lds)
+// Bilinear lookup of beta (Sec. 3.4), once per ray by one lane.  The angles
+// and grid coordinates are computed in binary64 (theta = polar angle from +z
+// on a clamped grid over [0, pi]; phi = atan2 on a periodic grid from -pi).
+// Component k goes to beta_lds[k * BS].
+template <int DC, int BS>
+__device__ __forceinline__ void lookup_beta(const RenderParams& P, const float d[3], float* beta_lds)
 {
     const double dx = d[0], dy = d[1], dz = d[2];
-    double theta, phi;
-    if constexpr (L == 1) {
-        theta = atan2_lookup(sqrt(dx * dx + dy * dy), dz);
-        phi = atan2_lookup(dy, dx);
-    } else {
-        const bool odd = (s & 1) != 0;
-        const double ang = atan2_lookup(odd ? dy : sqrt(dx * dx + dy * dy), odd ? dx : dz);
-        const uint32_t lo = static_cast<uint32_t>(__double_as_longlong(ang));
-        const uint32_t hi = static_cast<uint32_t>(static_cast<uint64_t>(__double_as_longlong(ang)) >> 32);
-        // even lane -> theta, odd lane -> phi, exchanged within each pair
-        const uint32_t lo_o = dpp32<qperm(1, 0, 3, 2)>(lo);
-        const uint32_t hi_o = dpp32<qperm(1, 0, 3, 2)>(hi);
-        const double other = __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi_o) << 32) | lo_o));
-        theta = odd ? other : ang;
-        phi = odd ? ang : other;
-    }
+    const double theta = atan2_lookup(sqrt(dx * dx + dy * dy), dz);
+    const double phi = atan2_lookup(dy, dx);
 
     // grid coordinates: theta in [0, pi] and phi + pi in [0, 2 pi], scaled
     // by factors the host computes in binary64
@@ -429,15 +413,13 @@ __device__ __forceinline__ void lookup_beta(const RenderParams& P, const float d
     auto component = [&](int k) {
         float acc = 0.0f;
 #pragma unroll
-        for (int c = 0; c < 4; c += L) {
-            const int corner = c + (L == 1 ? 0 : s);
-            const uint32_t off = (texel[corner] * static_cast<uint32_t>(D) + k) * esz;
+        for (int c = 0; c < 4; ++c) {
+            const uint32_t off = (texel[c] * static_cast<uint32_t>(D) + k) * esz;
             const float v = P.beta_f16 ? widen(load_at<_Float16>(P.beta, off)) : load_at<float>(P.beta, off);
-            acc = fmaf(wgt[corner], v, acc);
+            acc = fmaf(wgt[c], v, acc);
         }
-        return grp_sum<L>(acc);
+        return acc;
     };
-    // component k goes to beta_lds[k * BS]
     if constexpr (DC == 8) {
         // each corner record (D contiguous values) in 16-byte loads (at
         // D = 16 this measured slower than per-component loads)
@@ -446,13 +428,12 @@ __device__ __forceinline__ void lookup_beta(const RenderParams& P, const float d
         for (int k = 0; k < DC; ++k)
             acc[k] = 0.0f;
 #pragma unroll
-        for (int c = 0; c < 4; c += L) {
-            const int corner = c + (L == 1 ? 0 : s);
-            const float w = wgt[corner];
+        for (int c = 0; c < 4; ++c) {
+            const float w = wgt[c];
             if (P.beta_f16) {
 #pragma unroll
                 for (int q = 0; q < DC / 8; ++q) {
-                    const uint4 raw = load_at<uint4>(P.beta, texel[corner] * (DC * 2u) + 16u * q);
+                    const uint4 raw = load_at<uint4>(P.beta, texel[c] * (DC * 2u) + 16u * q);
                     _Float16 h[8];
                     __builtin_memcpy(h, &raw, 16);
 #pragma unroll
@@ -462,7 +443,7 @@ __device__ __forceinline__ void lookup_beta(const RenderParams& P, const float d
             } else {
 #pragma unroll
                 for (int q = 0; q < DC / 4; ++q) {
-                    const float4 v = load_at<float4>(P.beta, texel[corner] * (DC * 4u) + 16u * q);
+                    const float4 v = load_at<float4>(P.beta, texel[c] * (DC * 4u) + 16u * q);
                     acc[4 * q + 0] = fmaf(w, v.x, acc[4 * q + 0]);
                     acc[4 * q + 1] = fmaf(w, v.y, acc[4 * q + 1]);
                     acc[4 * q + 2] = fmaf(w, v.z, acc[4 * q + 2]);
@@ -472,7 +453,7 @@ __device__ __forceinline__ void lookup_beta(const RenderParams& P, const float d
         }
 #pragma unroll
         for (int k = 0; k < DC; ++k)
-            beta_lds[k * BS] = grp_sum<L>(acc[k]);
+            beta_lds[k * BS] = acc[k];
     } else if constexpr (DC > 0) {
 #pragma unroll
         for (int k = 0; k < DC; ++k)
@@ -893,11 +874,11 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
         // direction weights from the world direction
         if constexpr (LIN) {
             // beta goes to the ray's LDS row (the L lanes write equal values)
-            lookup_beta<DC, L, 1>(P, d_w, s, DC > 0 ? lin : lin + 9 * P.D + 3);
+            lookup_beta<DC, 1>(P, d_w, DC > 0 ? lin : lin + 9 * P.D + 3);
             __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
             fold_decoder<DC, L>(P, s, lin);
         } else {
-            lookup_beta<DC, L, BS>(P, d_w, s, beta);
+            lookup_beta<DC, BS>(P, d_w, beta);
         }
         march_geometry<SKIP, NDC>(P, o_w, d_w, geo);
     }
@@ -1198,9 +1179,9 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) 
                 // wave 0: beta, wave 1: the march geometry
                 if (wave == 0) {
                     if constexpr (LIN)
-                        lookup_beta<DC, 1, 1>(P, d_w, 0, DC > 0 ? lin_row(lane) : lin_row(lane) + 9 * P.D + 3);
+                        lookup_beta<DC, 1>(P, d_w, DC > 0 ? lin_row(lane) : lin_row(lane) + 9 * P.D + 3);
                     else
-                        lookup_beta<DC, 1, 64>(P, d_w, 0, beta_smem + lane);
+                        lookup_beta<DC, 64>(P, d_w, beta_smem + lane);
                 } else {
                     march_geometry<SKIP, NDC>(P, o_w, d_w, geom[lane]);
                 }
