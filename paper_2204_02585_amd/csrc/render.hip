@@ -45,9 +45,9 @@ __device__ __forceinline__ T load_at(const void* base, uint32_t off)
 }
 
 // ---------------------------------------------------------------------------
-// lanes of one ray: L = 2 or 4 consecutive lanes inside a quad, exchanged
-// with DPP quad permutations, or L = 8 lanes of a half-row, whose two quads
-// also exchange through the half-row mirror (lane i <-> 7 - i); the group is
+// lanes of one ray: L = 4 consecutive lanes of a quad, exchanged with DPP
+// quad permutations, or L = 8 lanes of a half-row, whose two quads also
+// exchange through the half-row mirror (lane i <-> 7 - i); the group is
 // always entirely active or inactive
 
 constexpr int qperm(int a, int b, int c, int d) { return a | (b << 2) | (c << 4) | (d << 6); }
@@ -77,9 +77,7 @@ __device__ __forceinline__ float dppf(float x)
 template <int L>
 __device__ __forceinline__ float grp_next(float x)
 {
-    if constexpr (L == 2)
-        return dppf<qperm(1, 1, 3, 3)>(x);
-    else if constexpr (L == 4)
+    if constexpr (L == 4)
         return dppf<qperm(1, 2, 3, 3)>(x);
     else if constexpr (L == 8) {
         // lane 3 takes lane 4 from the other quad (7 - 3 = 4)
@@ -94,9 +92,7 @@ __device__ __forceinline__ float grp_next(float x)
 template <int L>
 __device__ __forceinline__ float grp_first(float x)
 {
-    if constexpr (L == 2)
-        return dppf<qperm(0, 0, 2, 2)>(x);
-    else if constexpr (L == 4)
+    if constexpr (L == 4)
         return dppf<qperm(0, 0, 0, 0)>(x);
     else if constexpr (L == 8) {
         // the upper quad reads lane 0 where the mirror put it, in lane 7
@@ -107,18 +103,6 @@ __device__ __forceinline__ float grp_first(float x)
         return x;
 }
 
-// value of the group's last lane
-template <int L>
-__device__ __forceinline__ int32_t grp_last(int32_t x)
-{
-    if constexpr (L == 2)
-        return static_cast<int32_t>(dpp32<qperm(1, 1, 3, 3)>(static_cast<uint32_t>(x)));
-    else if constexpr (L == 4)
-        return static_cast<int32_t>(dpp32<qperm(3, 3, 3, 3)>(static_cast<uint32_t>(x)));
-    else
-        return x;
-}
-
 // Exclusive prefix sum of q over the group (lane order) and the group total.
 template <int L>
 __device__ __forceinline__ void grp_scan(uint64_t q, int s, uint64_t& excl, uint64_t& total)
@@ -126,10 +110,6 @@ __device__ __forceinline__ void grp_scan(uint64_t q, int s, uint64_t& excl, uint
     if constexpr (L == 1) {
         excl = 0;
         total = q;
-    } else if constexpr (L == 2) {
-        const uint64_t other = dpp64<qperm(1, 0, 3, 2)>(q);
-        excl = s ? other : 0;
-        total = q + other;
     } else {
         const int sq = s & 3;
         uint64_t y = q;
@@ -672,6 +652,20 @@ struct SigmaRecord<float> {
     }
 };
 
+// Sample index just past the exit parameter t_exit of a leap: every sample
+// below it has t_k <= t_exit.  x = (t_exit - near) / dt is pulled in by
+// 2^-19 (x + |near| / dt), more than the binary32 rounding of x and of
+// t_k = near + k dt together (under 8 units of 2^-24 of those magnitudes);
+// a stratified sample k lies at or below t_{k+1} of the uniform grid, so it
+// lands one index earlier.  Non-positive x gives an index <= 0 (the caller
+// clamps), +inf stays +inf, NaN stays NaN.
+__device__ __forceinline__ float leap_index(const RenderParams& P, float t_exit)
+{
+    const float x = (t_exit - P.near_t) * P.inv_dt;
+    const float y = x * (1.0f - 0x1p-19f) - P.leap_slack;
+    return floorf(y) + (P.stratified ? 0.0f : 1.0f);
+}
+
 // First sample index a leap may land on after sample i, whose nearest nodes
 // are (c[0], c[1], c[2]) and whose plane `j` texel lies at Chebyshev
 // distance D > 0 from every texel with sigma^j != 0.  Every sample whose
@@ -679,8 +673,8 @@ struct SigmaRecord<float> {
 // plane's two axes the grid coordinate g = (p - bmin) scale moves affinely in
 // t (g = g0 + t ds), and the node index stays inside the square while g is
 // below c + D - 1/2 (or above c - D + 1/2 moving down).  The bound is pulled
-// in by `margin` texels (the binary32 position and rounding error of g) and
-// the result by one sample, so every skipped sample is inside the square.
+// in by `margin` texels (the binary32 position and rounding error of g), so
+// every sample up to the exit parameter is inside the square.
 // inv_ds[r] = 1 / ds[r], +inf for ds = 0, so that an axis the ray does not
 // move along never ends the run (a non-positive distance to the bound there
 // gives -inf or NaN, i.e. no leap or the other axis: never a longer one);
@@ -699,7 +693,7 @@ __device__ __forceinline__ int32_t leap_target(const RenderParams& P, int j, uin
     // plane 0 (xy) uses axes 0, 1; plane 1 (yz) 1, 2; plane 2 (zx) 2, 0
     const float t01 = fminf(t[0], t[1]), t12 = fminf(t[1], t[2]), t20 = fminf(t[2], t[0]);
     const float t_exit = j == 0 ? t01 : (j == 1 ? t12 : t20);
-    const float f = floorf((t_exit - P.near_t) * P.inv_dt) - 1.0f;
+    const float f = leap_index(P, t_exit);
     const float lo = static_cast<float>(i + 1), hi = static_cast<float>(P.n_samples);
     return static_cast<int32_t>(fminf(fmaxf(f, lo), hi));
 }
@@ -723,7 +717,7 @@ __device__ __forceinline__ int32_t leap_cells(const RenderParams& P, uint32_t D,
         const float bound = inv_ds[r] > 0.0f ? G * (c + Df) - 0.5f - margin : G * (c - Df + 1.0f) - 0.5f + margin;
         t_exit = fminf(t_exit, (bound - g0[r]) * inv_ds[r]);
     }
-    const float f = floorf((t_exit - P.near_t) * P.inv_dt) - 1.0f;
+    const float f = leap_index(P, t_exit);
     const float lo = static_cast<float>(i + 1), hi = static_cast<float>(P.n_samples);
     return static_cast<int32_t>(fminf(fmaxf(f, lo), hi));
 }
@@ -843,6 +837,7 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
                                            int32_t v, int32_t lane, float* const beta, float* const lin,
                                            const RayGeom* pre = nullptr)
 {
+    static_assert(L == 1 || L == 4 || L == 8, "one, four or eight lanes per ray");
     const int32_t s = (L == 1) ? 0 : (lane & (L - 1));
     const int64_t ray = (static_cast<int64_t>(view) * P.height + v) * P.width + u;
     const int32_t N = P.n_samples;
@@ -902,14 +897,7 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
     while (base <= i1 && tau <= static_cast<uint64_t>(P.tau_eps)) {
         const int32_t i = base + s;
         const bool in_range = i <= i1;
-        // t_{i+1}: the next lane's t, or for the group's last lane the first
-        // sample of the next chunk (which becomes this lane's next t)
         const float t_next_chunk = sample_t(P, stratified, ray_key, base + L + s);
-        const float t_first_next = grp_first<L>(t_next_chunk);
-        const float t_lane_next = grp_next<L>(t);
-        float tn = (s == L - 1) ? t_first_next : t_lane_next;
-        if (i + 1 >= N)
-            tn = P.far_t;
 
         float p[3];
 #pragma unroll
@@ -994,15 +982,27 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
             }
         }
         float q = 0.0f;
-        uint64_t Q = 0;
-        if (sigma > 0.0f) {
-            const float gap = fmaxf(0.0f, tn - t);
-            const float delta = gap * dn;
-            q = sigma * delta;
-            Q = fixed_q(q);
+        uint64_t excl = 0, total = 0;
+        // a chunk in which no lane of the wave is occupied adds nothing to
+        // the optical depth: the exchange of t and the scan are skipped (a
+        // wave-uniform branch, so every group is whole inside it)
+        if (L == 1 || __builtin_amdgcn_ballot_w64(sigma > 0.0f) != 0) {
+            // t_{i+1}: the next lane's t, or for the group's last lane the
+            // first sample of the next chunk
+            const float t_first_next = grp_first<L>(t_next_chunk);
+            const float t_lane_next = grp_next<L>(t);
+            float tn = (s == L - 1) ? t_first_next : t_lane_next;
+            if (i + 1 >= N)
+                tn = P.far_t;
+            uint64_t Q = 0;
+            if (sigma > 0.0f) {
+                const float gap = fmaxf(0.0f, tn - t);
+                const float delta = gap * dn;
+                q = sigma * delta;
+                Q = fixed_q(q);
+            }
+            grp_scan<L>(Q, s, excl, total);
         }
-        uint64_t excl, total;
-        grp_scan<L>(Q, s, excl, total);
         const uint64_t tau_i = tau + excl;
         // with one lane per ray the loop condition already guarantees
         // tau_i = tau <= tau_eps and i <= i1

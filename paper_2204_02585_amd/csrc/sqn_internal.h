@@ -37,9 +37,10 @@ struct RenderParams {
     uint32_t rec_bytes;       // bytes of one uvw record (3D values)
     int64_t tau_eps;          // floor(-ln(eps) 2^32), INT64_MAX for eps = 0
     uint64_t seed;
-    float inv_dt;             // 1 / dt (for the conservative box clip only)
+    float inv_dt;             // 1 / dt (conservative box clip and leap indices)
+    float leap_slack;         // 2^-19 |near| / dt: leap indices are pulled in by it
     // launch geometry
-    int32_t lanes;            // lanes per ray: 1, 2 or 4
+    int32_t lanes;            // lanes per ray: 1, 4 or 8
     int32_t skip;             // 1: one lane per ray with empty-space leaps
     float leap_margin;        // texels a leap keeps from its square's edge
     int32_t tiles_x, tiles_y; // workgroup tiles per view

@@ -123,6 +123,25 @@ def test_camera_inside_box_and_axis_rays(mode):
     assert ref["n_inbox"].sum() > 0
 
 
+@pytest.mark.parametrize("name,mode", [("tiny", "skip1"), ("tiny", "skip4"), ("tiny", "skip8"),
+                                       ("tiny_alt", "skip4")])
+@pytest.mark.parametrize("stratified", [False, True])
+@pytest.mark.parametrize("case", ["dense", "sparse", "far_camera", "near_zero"])
+def test_leaps_land_past_empty_runs(case, stratified, name, mode):
+    """A leap lands on the first sample past the run that a distance field
+    (per plane, or the Eq. 5 cell grid) proves empty: no occupied sample may
+    be skipped, with many samples per texel, several texels per sample, a
+    large |near| / dt (the landing index's rounding slack) or near = 0."""
+    radius, near, far, N = {"dense": (4.0, 2.0, 6.0, 2048), "sparse": (4.0, 2.0, 6.0, 24),
+                            "far_camera": (60.0, 57.5, 62.5, 512), "near_zero": (4.0, 0.0, 8.0, 300)}[case]
+    sc = _small(name, width=32, height=32, n_samples=N, focal=10.0 * radius, stratified=stratified)
+    sc = dataclasses.replace(sc, near=near, far=far, poses=scenes.look_at_pose(radius, 45.0, 30.0)[None])
+    gpu = pu.gpu_render(sc, mode=mode)
+    ref = oracle.render_scene(sc)
+    pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), f"leaps {case}")
+    assert ref["n_occ"].sum() > 0
+
+
 @pytest.mark.parametrize("mode", MODES)
 def test_dense_scene_terminates(mode):
     """sigma_max 2000: most rays stop within a few samples."""
