@@ -118,6 +118,19 @@ def memory_ceilings(cache_bytes):
     return out
 
 
+def mfma_ceiling():
+    """Dense binary16 matrix-core rate of this GPU at two waves per SIMD
+    (independent 32x32x16 products, libsqn_probe.so), TFLOP/s."""
+    import ctypes
+    from paper_2204_02585_amd import build as _build
+    lib = ctypes.CDLL(_build.PROBE_PATH)
+    lib.sqn_probe_mfma_f16.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
+    tf = ctypes.c_float()
+    if lib.sqn_probe_mfma_f16(2000, ctypes.byref(tf)) != 0:
+        raise RuntimeError("matrix-core probe failed")
+    return round(tf.value, 1)
+
+
 def calibration_copies(dev):
     """Kernels of known traffic for scaling the hardware byte counters: a
     1 GiB fill and three 1 GiB device-to-device copies."""
@@ -209,6 +222,11 @@ def bench_generate(args):
                 "sample": f"{n_s} random position-grid points (binary64 numpy, BLAS threads as configured), "
                           f"{el:.1f} s wall"}
     nets.close()
+    ceilings = None
+    if not args.no_ceilings:
+        print("[bench] matrix-core ceiling", file=sys.stderr, flush=True)
+        peak = mfma_ceiling()
+        ceilings = {"mfma_f16_tflops": peak, "kernel_vs_mfma_ceiling": round(tflops / peak, 4)}
     out_line = {
         "metric": "cache generation: Mpoints/s of network evaluations on the cache grids",
         "value": round((n_pos + n_dir) / (ms * 1e-3) / 1e6, 2),
@@ -230,6 +248,7 @@ def bench_generate(args):
                      "traffic": measured_traffic(cfg.name, "generate"),
                      "algorithmic_flops_per_launch": int(flops), "kernel_ms_per_launch": round(ms, 4)},
         "cpu_baseline": base,
+        "ceilings": ceilings,
         "wall_s_timed": round(wall, 4),
     }
     print(json.dumps(out_line), flush=True)
@@ -248,7 +267,7 @@ def main():
                     help="march every sample (no leaps over empty space)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ceilings", action="store_true",
-                    help="skip the memory-level ceiling probes")
+                    help="skip the ceiling probes (memory levels; matrix cores for gen_*)")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB device-to-device 3 times (a kernel "

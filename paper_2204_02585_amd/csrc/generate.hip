@@ -16,9 +16,11 @@
 // is exact and no activation is shuffled.  Activations are rounded to
 // binary16 after bias and ReLU (binary32); accumulation is binary32.
 //
-// Per workgroup (4 waves, 128 points) the weights of each layer are staged
-// through LDS in chunks of 4 K steps x all M-tiles (32 KiB at 256 units);
-// each lane reads its 16-byte fragment with one ds_read_b128.
+// The weights of each layer are staged through LDS in chunks of 4 K steps
+// x all M-tiles (32 KiB at 256 units), shared by the waves of a workgroup
+// (8 waves, 256 points, for the position networks; 4 waves for the
+// direction network); each lane reads its 16-byte fragment with one
+// ds_read_b128.
 #include <math.h>
 
 #include "sqn_internal.h"
@@ -101,39 +103,44 @@ __device__ __forceinline__ void activate(const float16v (&acc)[T], const float* 
     }
 }
 
-// ---- double-buffered layers: while the matrix cores work on one chunk of
-// weights from LDS, the next chunk streams from global memory straight into
-// the other LDS buffer (global_load_lds, no registers); one barrier per
-// chunk, which also waits for those loads.
+// ---- double-buffered layers (position networks): while the matrix cores
+// work on one chunk of weights from LDS, the next chunk streams from global
+// memory straight into the other LDS buffer (global_load_lds, no
+// registers), and with a layer's first chunk its 256 biases; one barrier per
+// chunk, which also waits for those loads.  The two buffers are separate
+// arrays chosen at compile time, so the compiler sees that the reads of one
+// do not wait for the loads into the other.  Measured on the 1K cache:
+// biases read from global memory in the activation, loads left to sink to
+// the end of the chunk and one buffer array indexed at run time each cost
+// 4-10%; a deeper pipeline (four buffers, two chunks ahead) was slower.
 
-struct Stage {
-    _Float16* buf[2];
-    int cur;
-};
+constexpr int kPosThreads = 512;    // threads per position workgroup (2 waves per SIMD)
 
 // Direct-to-LDS loads of a chunk of TMAX tiles x 4 K steps (32 KiB at 8
 // tiles; the host pads every layer of the position networks to TMAX tiles):
-// piece i = 256 k + threadIdx.x (16 bytes) lands at buf + 16 i.
+// piece i = 512 k + threadIdx.x (16 bytes) lands at buf + 16 i.
 template <int TMAX>
 __device__ __forceinline__ void load_chunk(const _Float16* __restrict__ frag, _Float16* buf)
 {
     const int wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int k = 0; k < TMAX; ++k) {
-        const int piece = 256 * k + threadIdx.x;
+    for (int k = 0; k < TMAX * 256 / kPosThreads; ++k) {
+        const int piece = kPosThreads * k + threadIdx.x;
         __builtin_amdgcn_global_load_lds(reinterpret_cast<const unsigned int*>(frag) + 4 * piece,
-                                         reinterpret_cast<unsigned int*>(buf) + 4 * (256 * k + 64 * wave), 16, 0, 0);
+                                         reinterpret_cast<unsigned int*>(buf) + 4 * (kPosThreads * k + 64 * wave),
+                                         16, 0, 0);
     }
 }
 
 // One layer of KS K steps over `tiles` (<= TMAX) M-tiles for NB point
-// blocks.  The current chunk is in st.buf[st.cur] (loaded and published by
-// the last barrier); next_frag is the first chunk of the following layer
+// blocks.  The current chunk is in buffer P0 (loaded and published by the
+// last barrier); next_frag is the first chunk of the following layer
 // (after the last layer any valid chunk: loaded but never read).
-template <int TMAX, int NB, int KS>
+template <int TMAX, int NB, int KS, int P0>
 __device__ __forceinline__ void layer_pipe(const _Float16* __restrict__ frag, int tiles,
-                                           const half8 (&x)[NB][KS], float16v (&acc)[TMAX][NB], Stage& st,
-                                           const _Float16* next_frag)
+                                           const half8 (&x)[NB][KS], float16v (&acc)[TMAX][NB], _Float16* buf0,
+                                           _Float16* buf1, const _Float16* next_frag, const float* __restrict__ bias,
+                                           float* bias_lds)
 {
     const int lane = threadIdx.x & 63;
 #pragma unroll
@@ -145,9 +152,19 @@ __device__ __forceinline__ void layer_pipe(const _Float16* __restrict__ frag, in
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
         const bool last = c + 1 == NC;
-        load_chunk<TMAX>(last ? next_frag : frag + static_cast<size_t>(c + 1) * TMAX * kChunkSteps * kFrag,
-                         st.buf[st.cur ^ 1]);
-        const _Float16* wb = st.buf[st.cur];
+        // chunk c sits in buffer (P0 + c) % 2, known at compile time, so the
+        // compiler can tell the loads into the other buffer from the reads
+        _Float16* const cur = ((P0 + c) & 1) ? buf1 : buf0;
+        _Float16* const other = ((P0 + c) & 1) ? buf0 : buf1;
+        load_chunk<TMAX>(last ? next_frag : frag + static_cast<size_t>(c + 1) * TMAX * kChunkSteps * kFrag, other);
+        // the layer's 256 biases (1 KiB) follow the same way, by one wave
+        if (c == 0 && threadIdx.x < 64)
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const unsigned int*>(bias) + 4 * threadIdx.x,
+                                             reinterpret_cast<unsigned int*>(bias_lds), 16, 0, 0);
+        // keep the loads at the top of the chunk: issued late they would be
+        // waited for at the chunk's barrier
+        __builtin_amdgcn_sched_barrier(0);
+        const _Float16* wb = cur;
 #pragma unroll
         for (int ss = 0; ss < kChunkSteps; ++ss) {
             // fragment reads of the step ahead of its products, so each wait
@@ -171,7 +188,6 @@ __device__ __forceinline__ void layer_pipe(const _Float16* __restrict__ frag, in
             __builtin_amdgcn_sched_group_barrier(0x008, TMAX / 2 * NB, 0);
         }
         __syncthreads();
-        st.cur ^= 1;
     }
 }
 
@@ -229,11 +245,16 @@ __global__ void encode_axes(GenParams P, _Float16* __restrict__ tab)
 // plane's [n_p][n_p] grid per workgroup, row-major, kPosNB blocks of 32 per
 // wave (blocks share every weight fragment read from LDS).
 constexpr int kPosNB = 1;
-constexpr int kPosPoints = 4 * 32 * kPosNB;
+constexpr int kPosPoints = kPosThreads / 64 * 32 * kPosNB;
 
-__global__ __launch_bounds__(256, 2) void position_kernel(GenParams P, const _Float16* __restrict__ tab)
+__global__ __launch_bounds__(kPosThreads, 1) void position_kernel(GenParams P, const _Float16* __restrict__ tab)
 {
-    __shared__ __align__(16) _Float16 wbuf[2][8 * kChunkSteps * kFrag];
+    // two separate arrays, so that loads into one never wait for reads of
+    // the other
+    __shared__ __align__(16) _Float16 wbuf0[8 * kChunkSteps * kFrag];
+    __shared__ __align__(16) _Float16 wbuf1[8 * kChunkSteps * kFrag];
+    // layer l's biases sit in bias_lds[l & 1] from its first chunk on
+    __shared__ __align__(16) float bias_lds[2][256];
     const int j = blockIdx.y;
     const int lane = threadIdx.x & 63, h = lane >> 5;
     const int64_t n_pts = static_cast<int64_t>(P.n_p) * P.n_p;
@@ -246,11 +267,7 @@ __global__ __launch_bounds__(256, 2) void position_kernel(GenParams P, const _Fl
     // start loading the first layer's weights, then build the input
     // fragments: NeRF order [a, b, sin a, sin b, cos a, cos b, ...] per
     // frequency, zero beyond n_in (64 inputs = 4 K steps)
-    Stage st;
-    st.buf[0] = wbuf[0];
-    st.buf[1] = wbuf[1];
-    st.cur = 0;
-    load_chunk<8>(frag_of(net, 0), st.buf[0]);
+    load_chunk<8>(frag_of(net, 0), wbuf0);
     int64_t pt[kPosNB];
     half8 x0[kPosNB][4];
 #pragma unroll
@@ -282,19 +299,22 @@ __global__ __launch_bounds__(256, 2) void position_kernel(GenParams P, const _Fl
     float16v acc[8][kPosNB];
     half8 x[kPosNB][16];
     const int L = net.n_hidden;
-    layer_pipe<8, kPosNB, 4>(frag_of(net, 0), 8, x0, acc, st, frag_of(net, 1));
-    activate_nb<8, kPosNB>(acc, net.bias[0], x);
+    layer_pipe<8, kPosNB, 4, 0>(frag_of(net, 0), 8, x0, acc, wbuf0, wbuf1, frag_of(net, 1), net.bias[0],
+                                bias_lds[0]);
+    activate_nb<8, kPosNB>(acc, bias_lds[0], x);
     for (int l = 1; l < L; ++l) {
-        layer_pipe<8, kPosNB, 16>(frag_of(net, l), 8, x, acc, st, frag_of(net, l + 1));
-        activate_nb<8, kPosNB>(acc, net.bias[l], x);
+        layer_pipe<8, kPosNB, 16, 1>(frag_of(net, l), 8, x, acc, wbuf0, wbuf1, frag_of(net, l + 1),
+                                     net.bias[l], bias_lds[l & 1]);
+        activate_nb<8, kPosNB>(acc, bias_lds[l & 1], x);
     }
-    layer_pipe<8, kPosNB, 16>(frag_of(net, L), net.out_tiles, x, acc, st, frag_of(net, L));
+    layer_pipe<8, kPosNB, 16, 1>(frag_of(net, L), net.out_tiles, x, acc, wbuf0, wbuf1, frag_of(net, L),
+                                 net.bias[L], bias_lds[L & 1]);
 
     // head: pair slot P = 16 m + 8 gg + 4 h + q sits in rows 32 m + 16 gg +
     // 4 h + q and + 8 of tile m, i.e. accumulator entries 8 gg + q and
     // 8 gg + 4 + q of this lane; slot 0 is (sigma_0, w_sigma), slot 1 + c D + d
     // is (w_c[d], c_0[d]) (Eq. 3)
-    const float* hb = net.bias[L];
+    const float* hb = bias_lds[L & 1];
     const int D = P.D;
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
@@ -387,7 +407,7 @@ hipError_t launch_generate(const GenParams& p, _Float16* enc_table, hipStream_t 
     if (e != hipSuccess)
         return e;
     const int64_t n_pos = static_cast<int64_t>(p.n_p) * p.n_p;
-    position_kernel<<<dim3(static_cast<uint32_t>((n_pos + kPosPoints - 1) / kPosPoints), 3), 256, 0, stream>>>(
+    position_kernel<<<dim3(static_cast<uint32_t>((n_pos + kPosPoints - 1) / kPosPoints), 3), kPosThreads, 0, stream>>>(
         p, enc_table);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;

@@ -1,9 +1,11 @@
-// Memory-level ceilings for the render kernel's roofline, measured on the
-// GPU that runs it: streaming reads of a buffer (a footprint that one XCD's
-// L2 holds, one that the MALL holds, one that only HBM holds) and random
-// gathers of 64-byte records over a buffer, the access pattern of the cache
-// lookups.  A measurement aid for bench.py, built as its own library
-// (libsqn_probe.so); the render library does not use it.
+// Ceilings for the rooflines, measured on the GPU that runs the kernels:
+// for the render kernel, streaming reads of a buffer (a footprint that one
+// XCD's L2 holds, one that the MALL holds, one that only HBM holds) and
+// random gathers of 64-byte records over a buffer, the access pattern of the
+// cache lookups; for cache generation, the rate of independent
+// v_mfma_f32_32x32x16_f16 products at two waves per SIMD.  A measurement aid
+// for bench.py, built as its own library (libsqn_probe.so); the render
+// library does not use it.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -62,6 +64,31 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const uint4* __restric
     }
     if (acc == 0x9e3779b9u)
         sink[threadIdx.x] = acc;
+}
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float float16v __attribute__((ext_vector_type(16)));
+
+// Eight independent accumulators per wave, operands in registers: nothing
+// but the matrix cores limits the rate.
+__global__ __launch_bounds__(kThreads, 2) void mfma_kernel(int iters, float* __restrict__ sink)
+{
+    half8 a, b;
+    for (int e = 0; e < 8; ++e) {
+        a[e] = static_cast<_Float16>(static_cast<float>(threadIdx.x) * 0.001f + static_cast<float>(e));
+        b[e] = static_cast<_Float16>(0.5f * static_cast<float>(e));
+    }
+    float16v acc[8] = {};
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+        for (int m = 0; m < 8; ++m)
+            acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, acc[m], 0, 0, 0);
+    }
+    float s = 0.0f;
+    for (int m = 0; m < 8; ++m)
+        s += acc[m][0];
+    if (s == 1234.5f)
+        sink[threadIdx.x] = s;
 }
 
 int grid_for(uint64_t items)
@@ -154,6 +181,31 @@ int sqn_probe_gather(uint64_t bytes, uint64_t n_records, float* ms_out)
     (void)hipFree(sink);
     (void)hipFree(buf);
     return rc;
+}
+
+// Dense binary16 matrix-core rate: `iters` x 8 products of 32x32x16 per
+// wave, two workgroups of 4 waves on each CU, four rounds; *tflops_out in
+// TFLOP/s.  Returns 0, or 1 on a HIP error or bad argument.
+int sqn_probe_mfma_f16(int iters, float* tflops_out)
+{
+    if (iters < 1 || !tflops_out)
+        return 1;
+    int cus = 256;
+    int dev = 0;
+    if (hipGetDevice(&dev) == hipSuccess)
+        (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    float* sink = nullptr;
+    if (hipMalloc(reinterpret_cast<void**>(&sink), kThreads * 4) != hipSuccess)
+        return 1;
+    const int blocks = cus * 2 * 4;
+    float ms = 0.0f;
+    const int rc = time_launch([&] { mfma_kernel<<<blocks, kThreads>>>(iters, sink); }, &ms);
+    (void)hipFree(sink);
+    if (rc != 0 || !(ms > 0.0f))
+        return 1;
+    const double flops = static_cast<double>(blocks) * (kThreads / 64) * iters * 8 * (32.0 * 32.0 * 16.0 * 2.0);
+    *tflops_out = static_cast<float>(flops / (static_cast<double>(ms) * 1e-3) / 1e12);
+    return 0;
 }
 
 }  // extern "C"

@@ -127,8 +127,9 @@ def test_linear_decoder_validation_before_device_calls(lib):
 
 
 def test_probe_library_exports_and_rejects_bad_sizes():
-    """The benchmark's memory-ceiling probes (libsqn_probe.so) load and
-    reject sizes they cannot measure before touching the device."""
+    """The benchmark's ceiling probes (libsqn_probe.so: memory levels and
+    matrix cores) load and reject sizes they cannot measure before touching
+    the device."""
     from paper_2204_02585_amd import build
     raw = ctypes.CDLL(build.PROBE_PATH)
     raw.sqn_probe_stream.argtypes = [ctypes.c_uint64, ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
@@ -140,3 +141,6 @@ def test_probe_library_exports_and_rejects_bad_sizes():
     assert raw.sqn_probe_gather(100, 1, ctypes.byref(ms)) == 1
     assert raw.sqn_probe_gather(1 << 20, 0, ctypes.byref(ms)) == 1
     assert raw.sqn_probe_gather(64 << 32, 1, ctypes.byref(ms)) == 1
+    raw.sqn_probe_mfma_f16.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
+    assert raw.sqn_probe_mfma_f16(0, ctypes.byref(ms)) == 1
+    assert raw.sqn_probe_mfma_f16(10, None) == 1
