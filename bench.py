@@ -371,7 +371,10 @@ def main():
                    "empty_space_leaps": not args.dense},
         "frames_per_s": round(fps, 2),
         "samples": {"nominal_per_step": nominal, "live_inbox_per_step": live_inbox,
-                    "occupied_per_step": occupied},
+                    "occupied_per_step": occupied,
+                    "empty_fraction_of_live_inbox": round(1.0 - occupied / live_inbox, 4) if live_inbox else None,
+                    "live_inbox_msamples_per_s": round(live_inbox / (ms * 1e-3) / 1e6, 1),
+                    "occupied_msamples_per_s": round(occupied / (ms * 1e-3) / 1e6, 1)},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                      "traffic": (measured_traffic(cfg.name)
