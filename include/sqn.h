@@ -212,8 +212,13 @@ sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes);
  * within that empty square.  For the Eq. 5 decoder a texel of plane j counts
  * as empty when its s^j plus the largest s^k the other two planes hold along
  * the row or column the texel shares with them, plus b_sigma, is <= 0 in the
- * same binary32 order.  Only samples with sigma = 0 are skipped, so results,
- * sample counts and termination are those of the dense march.
+ * same binary32 order, and a 3-D grid of cells (at most 128 per axis) marks a
+ * cell empty when the three planes' largest s^j over its footprint, summed
+ * with b_sigma in that order, is <= 0; a sample in an empty cell reads no
+ * plane and leaps out of the empty cube around it.  Leaps land on the first
+ * sample that may lie past the proven-empty run.  Only samples with
+ * sigma = 0 are skipped, so results, sample counts and termination are those
+ * of the dense march.
  * Errors: SQN_ERR_INVALID_ARG. */
 sqn_status sqn_set_empty_space_skipping(sqn_caches* caches, int32_t enable);
 
