@@ -185,6 +185,29 @@ def test_two_streams_share_a_handle():
         caches.close()
 
 
+@pytest.mark.parametrize("mode", ["auto", "skip1", "L4"])
+def test_depth_output_is_optional(mode):
+    """depth_out may be NULL: the colours are those of a render with depth,
+    bit for bit."""
+    import torch
+    from paper_2204_02585_amd import binding
+    sc = _small("tiny", width=40, height=24)
+    caches = binding.caches_from_scene(sc)
+    try:
+        lanes, skip = pu.MODES[mode]
+        caches.set_lanes_per_ray(lanes)
+        caches.set_empty_space_skipping(skip)
+        P = torch.from_numpy(sc.poses).cuda()
+        rgb, depth = caches.render(P, sc.intrinsics, sc.near, sc.far, sc.config.n_samples)
+        rgb2, none = caches.render(P, sc.intrinsics, sc.near, sc.far, sc.config.n_samples, with_depth=False)
+        torch.cuda.synchronize()
+        assert none is None
+        assert torch.equal(rgb, rgb2)
+        assert float(depth.max()) > 0
+    finally:
+        caches.close()
+
+
 def test_empty_batch_is_noop():
     import torch
     from paper_2204_02585_amd import binding
