@@ -328,6 +328,17 @@ def main():
     wall = time.perf_counter() - wall0
     ms = ev0.elapsed_time(ev1) / args.steps
 
+    # spread over launches: the same launches again, each between two events
+    # (outside the timed region)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record(stream)
+    for i in range(args.steps):
+        caches.render(poses, scene.intrinsics, scene.near, scene.far, N, rgb, depth, stream=stream)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+    spread = {"median": round(per[len(per) // 2], 5), "min": round(per[0], 5), "max": round(per[-1], 5)}
+
     nominal = cfg.nominal_samples
     msps = nominal / (ms * 1e-3) / 1e6
     fps = B / (ms * 1e-3)
@@ -356,6 +367,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 5),
+        "ms_per_launch": spread,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
