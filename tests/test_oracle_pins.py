@@ -568,6 +568,94 @@ def test_stratified_first_interval_starts_at_jittered_sample():
     assert abs(r["acc"] - (1 - math.exp(-sig * (far - t0)))) < 1e-6
 
 
+def _golden_splitmix_seed0():
+    with open(os.path.join(GOLDEN, "splitmix64_seed0.txt")) as f:
+        return [int(l, 16) for l in f if l.strip() and not l.startswith("#")]
+
+
+def _jittered_t(near, far, N, i, h):
+    """Sample i of a stratified ray in binary32, one rounding per operation:
+    x = i + xi, t = near + x dt with dt = (far - near) / N and xi the top 24
+    bits of the SplitMix64 output h (the reading of Sec. 3.1's N samples
+    between the near and far planes with one seeded offset per bin)."""
+    f32 = np.float32
+    dt = f32(f32(far) - f32(near)) / f32(N)
+    xi = f32((h >> 40) * 2.0 ** -24)
+    x = f32(f32(i) + xi)
+    return f32(f32(near) + f32(x * dt))
+
+
+# three pixels in a row, all with the ray direction (0, 1, 0): the pose's
+# first two columns are zero, so a and b drop out and |d| = 1 for every pixel
+ROW3 = dict(fx=1.0, fy=1.0, cx=1.5, cy=0.5, width=3, height=1)
+ROW2 = dict(fx=1.0, fy=1.0, cx=1.0, cy=0.5, width=2, height=1)
+
+
+def test_stratified_offset_per_ray():
+    """One sample per ray (N = 1): ray r = u of a 3x1 image takes SplitMix64
+    output number r of the seed (counter = ray id N + i), so its single
+    interval is [t_0(r), far] and its opacity 1 - exp(-sigma (far - t_0(r)))
+    (Eq. 1 with one sample).  A counter that ignores the ray id gives all
+    three pixels output 0."""
+    h = _golden_splitmix_seed0()
+    near, far, sig = 2.0, 4.0, 0.5
+    out = oracle.render(const_planes(2, (sig, 1.0, 1.0)), uvw_const(2, 1, [(0, 0, 0)] * 3),
+                        beta_const(0.0), centre_ray_pose((0, 1, 0), (0, 0, 0)), ROW3,
+                        near, far, 1, (-100, -100, -100), (100, 100, 100), t_eps=0.0,
+                        stratified=True, seed=0)
+    accs = []
+    for r in range(3):
+        t0 = float(_jittered_t(near, far, 1, 0, h[r]))
+        want = -math.expm1(-sig * (far - t0))
+        assert abs(out[r]["acc"] - want) < 1e-12, r
+        assert abs(out[r]["depth"] - want * t0) < 1e-12, r
+        accs.append(out[r]["acc"])
+    # the three golden outputs give three different offsets
+    assert len(set(accs)) == 3
+
+
+def test_stratified_counter_steps_by_samples_per_ray():
+    """Two samples per ray on a 2x1 image: ray 1 starts at counter
+    1 N + 0 = 2, so its first sample uses output number 2, and with uniform
+    sigma the intervals telescope to far - t_0 whatever the second offset is.
+    A counter of ray id + i (output 1) or of i alone (output 0) fails."""
+    h = _golden_splitmix_seed0()
+    near, far, sig = 2.0, 4.0, 0.5
+    out = oracle.render(const_planes(2, (sig, 1.0, 1.0)), uvw_const(2, 1, [(0, 0, 0)] * 3),
+                        beta_const(0.0), centre_ray_pose((0, 1, 0), (0, 0, 0)), ROW2,
+                        near, far, 2, (-100, -100, -100), (100, 100, 100), t_eps=0.0,
+                        stratified=True, seed=0)
+    for r, k in ((0, 0), (1, 2)):
+        t0 = float(_jittered_t(near, far, 2, 0, h[k]))
+        # optical depth in 2^-32 fixed point: two truncations of at most 2^-32
+        assert abs(out[r]["acc"] + math.expm1(-sig * (far - t0))) < 1e-9, r
+
+
+def test_stratified_offset_per_sample_depth():
+    """Three samples of one ray (1x1 image) take SplitMix64 outputs 0, 1, 2
+    (counter = 0 N + i).  With uniform sigma and |d| = 1 the weights are
+    w_i = exp(-sigma (t_i - t_0)) (1 - exp(-sigma (t_{i+1} - t_i))), t_3 = far
+    (Eq. 1 with the exclusive T_i), and depth = sum_i w_i t_i.  A counter that
+    ignores i puts all three samples at the same offset."""
+    h = _golden_splitmix_seed0()
+    # sigma = 1/2 keeps q_i = sigma delta_i exact in binary32
+    near, far, N, sig = 2.0, 5.0, 3, 0.5
+    r = oracle.render(const_planes(2, (sig, 1.0, 1.0)), uvw_const(2, 1, [(0, 0, 0)] * 3),
+                      beta_const(0.0), centre_ray_pose((0, 1, 0), (0, 0, 0)), ONE_PIXEL,
+                      near, far, N, (-100, -100, -100), (100, 100, 100), t_eps=0.0,
+                      stratified=True, seed=0)[0]
+    t = [float(_jittered_t(near, far, N, i, h[i])) for i in range(N)] + [far]
+    depth = acc = 0.0
+    for i in range(N):
+        w = math.exp(-sig * (t[i] - t[0])) * -math.expm1(-sig * (t[i + 1] - t[i]))
+        depth += w * t[i]
+        acc += w
+    assert abs(r["acc"] - acc) < 1e-9
+    assert abs(r["depth"] - depth) < 1e-8
+    # the hand-derived offsets are those of the golden outputs, not equal
+    assert len({t[1] - t[0], t[2] - t[1], t[3] - t[2]}) == 3
+
+
 # --------------------------------------------------------------------------
 # Sec. 3.4: bilinear direction lookup over (theta, phi)
 # --------------------------------------------------------------------------
