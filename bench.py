@@ -70,11 +70,54 @@ def measured_traffic(config_name, kind="render"):
     return int(rec["traffic_bytes_per_launch"])
 
 
+# Worker threads a process on a one-GPU share of the shared host may use.
+HOST_CPU_SHARE = 16
+
+
+def host_description():
+    """The host the CPU baseline runs on: logical CPUs, the CPUs this
+    process may run on, physical cores and the CPU model (/proc/cpuinfo)."""
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        affinity = os.cpu_count() or 1
+    model, cores = None, set()
+    try:
+        phys = core = None
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                key, _, val = line.partition(":")
+                key, val = key.strip(), val.strip()
+                if key == "model name" and model is None:
+                    model = val
+                elif key == "physical id":
+                    phys = val
+                elif key == "core id":
+                    core = val
+                elif not key and phys is not None and core is not None:
+                    cores.add((phys, core))
+                    phys = core = None
+        if phys is not None and core is not None:
+            cores.add((phys, core))
+    except OSError:
+        pass
+    return {"host_logical_cpus": os.cpu_count(), "affinity_cpus": affinity,
+            "host_physical_cores": len(cores) or None, "cpu_model": model}
+
+
+def baseline_threads():
+    """All CPUs this process may run on, up to the CPU share of one GPU."""
+    return max(1, min(HOST_CPU_SHARE, host_description()["affinity_cpus"]))
+
+
 def cpu_baseline(scene, budget_s=12.0, max_frames=40):
     """The CPU oracle as it stands, on whole frames of the same workload,
-    repeated until ~budget_s of wall time (at least one frame)."""
+    repeated until ~budget_s of wall time (at least one frame).  Threads:
+    every CPU the process may use, capped at the host's CPU share for one
+    GPU (HOST_CPU_SHARE)."""
     import oracle
-    threads = min(16, os.cpu_count() or 1)
+    host = host_description()
+    threads = baseline_threads()
     cfg = scene.config
     frames = 0
     t0 = time.perf_counter()
@@ -87,7 +130,8 @@ def cpu_baseline(scene, budget_s=12.0, max_frames=40):
     samples = frames * cfg.width * cfg.height * cfg.n_samples
     return {"value": samples / el / 1e6, "unit": "Msamples/s", "cores": threads, "kind": "oracle",
             "sample": f"{frames} full {cfg.width}x{cfg.height}x{cfg.n_samples} frame(s) of view 0, "
-                      f"{el:.1f} s wall", "frames_per_s": frames / el}
+                      f"{el:.1f} s wall", "frames_per_s": frames / el,
+            "threads": threads, "thread_cap": HOST_CPU_SHARE, **host}
 
 
 def memory_ceilings(cache_bytes):
@@ -220,7 +264,7 @@ def bench_generate(args):
         threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or (os.cpu_count() or 1)
         base = {"value": round(n_s / el / 1e6, 4), "unit": "Mpoints/s", "cores": threads, "kind": "oracle",
                 "sample": f"{n_s} random position-grid points (binary64 numpy, BLAS threads as configured), "
-                          f"{el:.1f} s wall"}
+                          f"{el:.1f} s wall", "threads": threads, **host_description()}
     nets.close()
     ceilings = None
     if not args.no_ceilings:

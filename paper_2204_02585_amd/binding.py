@@ -139,9 +139,74 @@ def _stream(stream) -> ctypes.c_void_p:
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def _poses_arg(poses: torch.Tensor) -> torch.Tensor:
+    """float32 [B,3,4] camera-to-world on a CUDA device, contiguous; [B,4,4]
+    poses lose their last row."""
+    if poses.dtype != torch.float32:
+        raise TypeError(f"poses must be float32, got {poses.dtype}")
+    if poses.device.type != "cuda":
+        raise ValueError("poses must live on a CUDA device")
+    if poses.dim() != 3 or poses.shape[1:] not in ((3, 4), (4, 4)):
+        raise ValueError(f"poses must have shape [B,3,4] (or [B,4,4]), got {tuple(poses.shape)}")
+    return poses[:, :3, :].contiguous()
+
+
+def _output_arg(t: torch.Tensor, shape, device, name: str) -> None:
+    if t.dtype != torch.float32 or tuple(t.shape) != tuple(shape) or not t.is_contiguous() or t.device != device:
+        raise ValueError(f"{name} must be a contiguous float32 tensor of shape {tuple(shape)} on {device}")
+
+
 def _intrinsics(intr: dict) -> Intrinsics:
     return Intrinsics(float(intr["fx"]), float(intr["fy"]), float(intr["cx"]), float(intr["cy"]),
                       int(intr["width"]), int(intr["height"]))
+
+
+def _cache_args(sigma, uvw, beta, bbox_min, bbox_max, t_eps, stratified, seed, stream):
+    """sqn_cache_desc and plane pointer arrays for cache tensors on one
+    device.  Copies made to make a tensor contiguous are ordered before the
+    library's work on `stream`."""
+    sigma = [s.contiguous() for s in sigma]
+    uvw = [u.contiguous() for u in uvw]
+    beta = beta.contiguous()
+    dev = beta.device
+    if len(sigma) != 3 or len(uvw) != 3:
+        raise ValueError("three sigma planes and three uvw planes are needed (xy, yz, zx)")
+    for t in (*sigma, *uvw, beta):
+        if t.device != dev or dev.type != "cuda":
+            raise ValueError("cache tensors must all live on one CUDA device")
+    n_p, D = sigma[0].shape[0], uvw[0].shape[-1] // 3
+    if (any(t.shape[:2] != (n_p, n_p) or t.dtype != sigma[0].dtype or t.dim() != sigma[0].dim() for t in sigma)
+            or any(t.shape != (n_p, n_p, 3 * D) or t.dtype != uvw[0].dtype for t in uvw)
+            or uvw[0].shape[-1] % 3 != 0 or beta.dim() != 3 or beta.shape[2] != D):
+        raise ValueError("cache shapes: sigma [n_p, n_p] (or [n_p, n_p, D_sigma]), uvw [n_p, n_p, 3D], "
+                         "beta [n_theta, n_phi, D], one dtype per kind")
+    _order_after_current(stream, *sigma, *uvw, beta)
+    desc = CacheDesc()
+    desc.n_p, desc.D = sigma[0].shape[0], uvw[0].shape[-1] // 3
+    desc.n_theta, desc.n_phi = beta.shape[0], beta.shape[1]
+    desc.sigma_dtype, desc.uvw_dtype, desc.beta_dtype = (_dtype_code(sigma[0]), _dtype_code(uvw[0]),
+                                                         _dtype_code(beta))
+    desc.stratified = 1 if stratified else 0
+    for r in range(3):
+        desc.bbox_min[r] = bbox_min[r]
+        desc.bbox_max[r] = bbox_max[r]
+    desc.t_eps = t_eps
+    desc.reserved = 0
+    desc.seed = int(seed) & 0xFFFFFFFFFFFFFFFF
+    sp = (ctypes.c_void_p * 3)(*[t.data_ptr() for t in sigma])
+    up = (ctypes.c_void_p * 3)(*[t.data_ptr() for t in uvw])
+    return desc, sigma, uvw, beta, sp, up
+
+
+def _order_after_current(stream, *tensors) -> None:
+    """Make `stream` wait for the work already queued on torch's current
+    stream (the copies .contiguous() or .to() may just have queued there),
+    and tell torch's allocator that `tensors` are in use on `stream`."""
+    if stream is not None and stream != torch.cuda.current_stream():
+        stream.wait_stream(torch.cuda.current_stream())
+        for t in tensors:
+            if t is not None:
+                t.record_stream(stream)
 
 
 class Caches:
@@ -154,26 +219,10 @@ class Caches:
                  beta: torch.Tensor, bbox_min, bbox_max, t_eps: float = 1e-4,
                  stratified: bool = False, seed: int = 0, stream=None, decoder=None):
         self._h = ctypes.c_void_p(None)
-        sigma = [s.contiguous() for s in sigma]
-        uvw = [u.contiguous() for u in uvw]
-        beta = beta.contiguous()
-        n_p = sigma[0].shape[0]
-        D = uvw[0].shape[-1] // 3
-        desc = CacheDesc()
-        desc.n_p, desc.D = n_p, D
-        desc.n_theta, desc.n_phi = beta.shape[0], beta.shape[1]
-        desc.sigma_dtype, desc.uvw_dtype, desc.beta_dtype = (_dtype_code(sigma[0]), _dtype_code(uvw[0]),
-                                                             _dtype_code(beta))
-        desc.stratified = 1 if stratified else 0
-        for r in range(3):
-            desc.bbox_min[r] = bbox_min[r]
-            desc.bbox_max[r] = bbox_max[r]
-        desc.t_eps = t_eps
-        desc.reserved = 0
-        desc.seed = int(seed) & 0xFFFFFFFFFFFFFFFF
+        desc, sigma, uvw, beta, sp, up = _cache_args(sigma, uvw, beta, bbox_min, bbox_max, t_eps,
+                                                     stratified, seed, stream)
         self.desc = desc
-        sp = (ctypes.c_void_p * 3)(*[s.data_ptr() for s in sigma])
-        up = (ctypes.c_void_p * 3)(*[u.data_ptr() for u in uvw])
+        D = desc.D
         if decoder is None:
             _check(lib.sqn_create_caches(ctypes.byref(desc), sp, up, _ptr(beta), _stream(stream),
                                          ctypes.byref(self._h)))
@@ -230,14 +279,20 @@ class Caches:
     def render(self, poses: torch.Tensor, intrinsics: dict, near: float, far: float,
                n_samples: int, rgb_out: Optional[torch.Tensor] = None,
                depth_out: Optional[torch.Tensor] = None, with_depth: bool = True, stream=None):
-        """sqn_render; returns (rgb [B,H,W,3], depth [B,H,W] or None)."""
-        poses = poses.contiguous()
+        """sqn_render; returns (rgb [B,H,W,3], depth [B,H,W] or None).
+        poses: float32 [B,3,4] camera-to-world (or [B,4,4], whose last row is
+        dropped) on the caches' device."""
+        poses = _poses_arg(poses)
         B = poses.shape[0]
         H, W = int(intrinsics["height"]), int(intrinsics["width"])
         if rgb_out is None:
             rgb_out = torch.empty((B, H, W, 3), dtype=torch.float32, device=poses.device)
         if depth_out is None and with_depth:
             depth_out = torch.empty((B, H, W), dtype=torch.float32, device=poses.device)
+        _output_arg(rgb_out, (B, H, W, 3), poses.device, "rgb_out")
+        if depth_out is not None:
+            _output_arg(depth_out, (B, H, W), poses.device, "depth_out")
+        _order_after_current(stream, poses, rgb_out, depth_out)
         intr = _intrinsics(intrinsics)
         _check(lib.sqn_render(self.handle, _ptr(poses), B, ctypes.byref(intr), float(near),
                               float(far), int(n_samples), _ptr(rgb_out), _ptr(depth_out),
@@ -247,13 +302,14 @@ class Caches:
     def render_stats(self, poses: torch.Tensor, intrinsics: dict, near: float, far: float,
                      n_samples: int, stream=None):
         """sqn_render_stats; returns (rgb, depth, stats [B,H,W,4] int32 view of
-        {stop, n_inbox, n_occ, hash})."""
-        poses = poses.contiguous()
+        {stop, n_inbox, n_occ, hash}).  poses as for render()."""
+        poses = _poses_arg(poses)
         B = poses.shape[0]
         H, W = int(intrinsics["height"]), int(intrinsics["width"])
         rgb = torch.empty((B, H, W, 3), dtype=torch.float32, device=poses.device)
         depth = torch.empty((B, H, W), dtype=torch.float32, device=poses.device)
         stats = torch.empty((B, H, W, 4), dtype=torch.int32, device=poses.device)
+        _order_after_current(stream, poses, rgb, depth, stats)
         intr = _intrinsics(intrinsics)
         _check(lib.sqn_render_stats(self.handle, _ptr(poses), B, ctypes.byref(intr), float(near),
                                     float(far), int(n_samples), _ptr(rgb), _ptr(depth),
