@@ -158,6 +158,35 @@ sqn_status sqn_create_linear_caches(const sqn_cache_desc* desc,
                                     void* stream,
                                     sqn_caches** out);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops that swap scenes, harnesses that forbid hipMalloc):
+ * sqn_create_caches into the device memory an existing handle already owns,
+ * allocating nothing.  The handle (made by sqn_create_caches, Eq. 4) then
+ * holds the caches desc describes; its lanes, leap and NDC settings stay.
+ *   caches:      the handle; its device block must hold the new layout
+ *                (sqn_cache_device_bytes of a handle created from desc);
+ *   desc, sigma_planes, uvw_planes, beta: as for sqn_create_caches, with
+ *                n_p <= 2048;
+ *   stream:      hipStream_t the work is ordered on.
+ * Unlike sqn_create_caches the call does not wait: the input arrays must
+ * stay valid, and no render with the handle may run on another stream, until
+ * the stream has finished the call's work; renders on `stream` after it see
+ * the new caches.  The preparation uses a 20 MiB scratch array that each
+ * device holds for the life of the process and that every call on that
+ * device shares: calls on one device that overlap in time (two streams, two
+ * threads) race on it and must be serialised by the caller.
+ * Errors: SQN_ERR_INVALID_ARG (NULL, range, n_p > 2048, a layout larger than
+ * the handle's block, input arrays that are not device allocations large
+ * enough, wrong device), SQN_ERR_UNSUPPORTED (a handle made by
+ * sqn_create_linear_caches, or a uvw plane or direction cache of 2^32 bytes
+ * or more), SQN_ERR_DEVICE (a launch failed: the handle's contents are then
+ * unspecified; destroy it or recreate it again). */
+sqn_status sqn_recreate_caches(sqn_caches* caches, const sqn_cache_desc* desc,
+                               const void* const sigma_planes[3],
+                               const void* const uvw_planes[3],
+                               const void* beta,
+                               void* stream);
+
 /* Render n_poses views (Sec. 3.4, Eq. 1).
  *   poses:      device pointer, [n_poses][3][4] binary32 camera-to-world;
  *   intrinsics: host pointer, read during the call only;

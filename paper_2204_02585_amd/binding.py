@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libsqn.so")
 SQN_OK, SQN_ERR_INVALID_ARG, SQN_ERR_OUT_OF_MEMORY, SQN_ERR_DEVICE, SQN_ERR_UNSUPPORTED = range(5)
 SQN_F32, SQN_F16 = 0, 1
 
-EXPORTS = ("sqn_create_caches", "sqn_create_linear_caches", "sqn_render", "sqn_render_stats",
+EXPORTS = ("sqn_create_caches", "sqn_create_linear_caches", "sqn_recreate_caches", "sqn_render", "sqn_render_stats",
            "sqn_set_lanes_per_ray", "sqn_set_empty_space_skipping", "sqn_set_ndc", "sqn_cache_device_bytes",
            "sqn_destroy", "sqn_status_string", "sqn_last_error", "sqn_create_networks",
            "sqn_generate_caches", "sqn_networks_device_bytes", "sqn_destroy_networks")
@@ -73,6 +73,9 @@ def _load() -> ctypes.CDLL:
     lib.sqn_create_linear_caches.argtypes = [ctypes.POINTER(CacheDesc), ctypes.POINTER(LinearDecoder),
                                              ctypes.POINTER(vp), ctypes.POINTER(vp), vp, vp,
                                              ctypes.POINTER(vp)]
+    lib.sqn_recreate_caches.restype = ctypes.c_int
+    lib.sqn_recreate_caches.argtypes = [vp, ctypes.POINTER(CacheDesc), ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                        vp, vp]
     lib.sqn_create_networks.restype = ctypes.c_int
     lib.sqn_create_networks.argtypes = [ctypes.POINTER(MLPDesc), ctypes.POINTER(MLPDesc), i32, i32, i32,
                                         vp, ctypes.POINTER(vp)]
@@ -247,6 +250,17 @@ class Caches:
         if not self._h:
             raise ValueError("caches have been destroyed")
         return self._h
+
+    def recreate(self, sigma: Sequence[torch.Tensor], uvw: Sequence[torch.Tensor], beta: torch.Tensor,
+                 bbox_min, bbox_max, t_eps: float = 1e-4, stratified: bool = False, seed: int = 0,
+                 stream=None) -> None:
+        """sqn_recreate_caches: new Eq. 4 caches in this handle's device
+        memory, without allocating; the tensors must stay alive until
+        `stream` has finished the call's work."""
+        desc, sigma, uvw, beta, sp, up = _cache_args(sigma, uvw, beta, bbox_min, bbox_max, t_eps,
+                                                     stratified, seed, stream)
+        _check(lib.sqn_recreate_caches(self.handle, ctypes.byref(desc), sp, up, _ptr(beta), _stream(stream)))
+        self.desc = desc
 
     @property
     def device_bytes(self) -> int:

@@ -8,7 +8,7 @@
 #include <string.h>
 
 #include <limits>
-#include <string>
+#include <mutex>
 #include <vector>
 
 #include "sqn_internal.h"
@@ -48,20 +48,22 @@ struct sqn_networks {
 
 namespace {
 
-thread_local std::string g_last_error;
+// detail of the last failure on this thread; a fixed buffer, so that no
+// error path allocates
+thread_local char g_last_error[512];
 
 sqn_status fail(sqn_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 
 sqn_status fail(sqn_status s, const char* fmt, ...)
 {
-    char buf[512];
     va_list ap;
     va_start(ap, fmt);
-    vsnprintf(buf, sizeof(buf), fmt, ap);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
     va_end(ap);
-    g_last_error = buf;
     return s;
 }
+
+void clear_error() { g_last_error[0] = '\0'; }
 
 size_t dtype_size(int32_t dt) { return dt == SQN_F16 ? 2 : 4; }
 
@@ -312,6 +314,47 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
     return SQN_OK;
 }
 
+size_t align256(size_t x) { return (x + 255) & ~size_t{255}; }
+
+// Where each array of a handle lives in its device block (offsets from the
+// block start, each region 256-byte aligned) and the block size.
+struct CacheLayout {
+    size_t packed_bytes, uvw_bytes, beta_bytes, lin_bytes, cells;
+    size_t off_sigma[3], off_uvw[3], off_beta, off_lin, off_cells, total;
+};
+
+CacheLayout cache_layout(const sqn_cache_desc* desc, bool linear)
+{
+    CacheLayout L;
+    const int32_t D = desc->D;
+    const size_t texels = static_cast<size_t>(desc->n_p) * desc->n_p;
+    // packed records: 4 bytes for binary16 sigma, 8 for binary32 sigma or
+    // the linear decoder's binary32 partial sums
+    L.packed_bytes = texels * (!linear && desc->sigma_dtype == SQN_F16 ? 4 : 8);
+    L.uvw_bytes = texels * 3 * D * dtype_size(desc->uvw_dtype);
+    L.beta_bytes = static_cast<size_t>(desc->n_theta) * desc->n_phi * D * dtype_size(desc->beta_dtype);
+    L.lin_bytes = linear ? (9 * static_cast<size_t>(D) + 3) * D * sizeof(float) : 0;
+    const int32_t cell_m = sqn::linear_cells(desc->n_p);
+    L.cells = linear ? static_cast<size_t>(cell_m) * cell_m * cell_m : 0;
+    size_t total = 0;
+    for (int j = 0; j < 3; ++j) {
+        L.off_sigma[j] = total;
+        total += align256(L.packed_bytes);
+    }
+    for (int j = 0; j < 3; ++j) {
+        L.off_uvw[j] = total;
+        total += align256(L.uvw_bytes);
+    }
+    L.off_beta = total;
+    total += align256(L.beta_bytes);
+    L.off_lin = total;
+    total += align256(L.lin_bytes);
+    L.off_cells = total;
+    total += align256(L.cells);
+    L.total = total;
+    return L;
+}
+
 // Shared body of the two create calls; dec == NULL selects Eq. 4.
 sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec,
                        const void* const sigma_planes[3], const void* const uvw_planes[3],
@@ -333,17 +376,12 @@ sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec
     const int32_t ds = linear ? dec->d_sigma : 1;
     const size_t texels = static_cast<size_t>(desc->n_p) * desc->n_p;
     const size_t sigma_bytes = texels * ds * dtype_size(desc->sigma_dtype);
-    // packed records: 4 bytes for binary16 sigma, 8 for binary32 sigma or
-    // the linear decoder's binary32 partial sums
-    const size_t packed_bytes = texels * (!linear && desc->sigma_dtype == SQN_F16 ? 4 : 8);
-    const size_t uvw_bytes = texels * 3 * D * dtype_size(desc->uvw_dtype);
-    const size_t beta_bytes = static_cast<size_t>(desc->n_theta) * desc->n_phi * D
-                              * dtype_size(desc->beta_dtype);
+    const CacheLayout lay = cache_layout(desc, linear);
+    const size_t uvw_bytes = lay.uvw_bytes, beta_bytes = lay.beta_bytes, lin_bytes = lay.lin_bytes;
     const size_t lin_rows = 9 * static_cast<size_t>(D) + 3;
-    const size_t lin_bytes = linear ? lin_rows * D * sizeof(float) : 0;
     const int32_t cell_shift = sqn::linear_cell_shift(desc->n_p);
     const int32_t cell_m = sqn::linear_cells(desc->n_p);
-    const size_t cells = linear ? static_cast<size_t>(cell_m) * cell_m * cell_m : 0;
+    const size_t cells = lay.cells;
     static const char* names_s[3] = {"sigma_planes[0] (xy)", "sigma_planes[1] (yz)", "sigma_planes[2] (zx)"};
     static const char* names_u[3] = {"uvw_planes[0] (xy)", "uvw_planes[1] (yz)", "uvw_planes[2] (zx)"};
     for (int j = 0; j < 3; ++j) {
@@ -355,22 +393,10 @@ sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec
     if ((s = check_device_range(beta, beta_bytes, "beta")) != SQN_OK)
         return s;
 
-    auto align = [](size_t x) { return (x + 255) & ~size_t{255}; };
-    size_t off_sigma[3], off_uvw[3], off_beta, off_lin, total = 0;
-    for (int j = 0; j < 3; ++j) {
-        off_sigma[j] = total;
-        total += align(packed_bytes);
-    }
-    for (int j = 0; j < 3; ++j) {
-        off_uvw[j] = total;
-        total += align(uvw_bytes);
-    }
-    off_beta = total;
-    total += align(beta_bytes);
-    off_lin = total;
-    total += align(lin_bytes);
-    const size_t off_cells = total;
-    total += align(cells);
+    auto align = align256;
+    const size_t* off_sigma = lay.off_sigma;
+    const size_t* off_uvw = lay.off_uvw;
+    const size_t off_beta = lay.off_beta, off_lin = lay.off_lin, off_cells = lay.off_cells, total = lay.total;
 
     // temporary buffers of the preparation, freed before returning
     size_t work_total = 0;
@@ -501,7 +527,49 @@ sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec
         h->cell_m = cell_m;
     }
     *out = h;
-    g_last_error.clear();
+    clear_error();
+    return SQN_OK;
+}
+
+// ---- sqn_recreate_caches: create-time preparation without allocating -------
+//
+// The distance transform of a plane needs n_p^2 bytes of live mask and two
+// n_p^2 arrays of uint16 (row and capped Chebyshev distances).  For callers
+// that cannot allocate, that scratch lives in one file-scope device array,
+// sized for n_p <= kRecreateMaxNp.  Every device the library runs on holds
+// its own copy until the process ends.  In host code `scratch` names a host
+// stand-in, not device memory: its device address is taken once per device
+// with hipGetSymbolAddress and only that address is passed to kernels.
+
+constexpr int32_t kRecreateMaxNp = 2048;
+constexpr size_t kRecreateScratchBytes = 5 * static_cast<size_t>(kRecreateMaxNp) * kRecreateMaxNp;
+static_assert(kRecreateScratchBytes == 20u << 20, "20 MiB of scratch");
+
+__device__ __align__(256) uint8_t scratch[kRecreateScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices];   // device address of `scratch` per device
+
+// Device address of `scratch` on the current device `device`, looked up on
+// the first call for that device.
+sqn_status scratch_address(int device, void** out)
+{
+    if (device < 0 || device >= kMaxDevices)
+        return fail(SQN_ERR_UNSUPPORTED, "device %d is beyond the %d devices this library tracks", device,
+                    kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[device]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || p == nullptr) {
+            (void)hipGetLastError();
+            return fail(SQN_ERR_DEVICE, "hipGetSymbolAddress(scratch) failed on device %d: %s", device,
+                        hipGetErrorString(e));
+        }
+        g_scratch_ptr[device] = p;
+    }
+    *out = g_scratch_ptr[device];
     return SQN_OK;
 }
 
@@ -621,6 +689,84 @@ sqn_status sqn_create_linear_caches(const sqn_cache_desc* desc, const sqn_linear
     return create_impl(desc, decoder, sigma_planes, uvw_planes, beta, stream, out);
 }
 
+sqn_status sqn_recreate_caches(sqn_caches* caches, const sqn_cache_desc* desc,
+                               const void* const sigma_planes[3], const void* const uvw_planes[3],
+                               const void* beta, void* stream)
+{
+    if (!caches)
+        return fail(SQN_ERR_INVALID_ARG, "caches is NULL");
+    sqn_status s = validate_desc(desc);
+    if (s != SQN_OK)
+        return s;
+    if (caches->linear)
+        return fail(SQN_ERR_UNSUPPORTED, "the handle holds Eq. 5 caches; sqn_recreate_caches takes Eq. 4 handles");
+    if (!sigma_planes || !uvw_planes)
+        return fail(SQN_ERR_INVALID_ARG, "plane pointer array is NULL");
+    if (desc->n_p > kRecreateMaxNp)
+        return fail(SQN_ERR_INVALID_ARG, "n_p = %d exceeds %d, the largest grid the static scratch (%zu bytes) covers",
+                    desc->n_p, kRecreateMaxNp, kRecreateScratchBytes);
+    int device = -1;
+    if (hipGetDevice(&device) != hipSuccess)
+        return fail(SQN_ERR_DEVICE, "hipGetDevice failed");
+    if (device != caches->device)
+        return fail(SQN_ERR_INVALID_ARG, "caches live on device %d, current device is %d", caches->device, device);
+    const CacheLayout lay = cache_layout(desc, false);
+    if (lay.total > caches->bytes)
+        return fail(SQN_ERR_INVALID_ARG, "the caches need %zu bytes of device memory, the handle holds %zu",
+                    lay.total, caches->bytes);
+    const size_t texels = static_cast<size_t>(desc->n_p) * desc->n_p;
+    const size_t sigma_bytes = texels * dtype_size(desc->sigma_dtype);
+    static const char* names_s[3] = {"sigma_planes[0] (xy)", "sigma_planes[1] (yz)", "sigma_planes[2] (zx)"};
+    static const char* names_u[3] = {"uvw_planes[0] (xy)", "uvw_planes[1] (yz)", "uvw_planes[2] (zx)"};
+    for (int j = 0; j < 3; ++j) {
+        if ((s = check_device_range(sigma_planes[j], sigma_bytes, names_s[j])) != SQN_OK)
+            return s;
+        if ((s = check_device_range(uvw_planes[j], lay.uvw_bytes, names_u[j])) != SQN_OK)
+            return s;
+    }
+    if ((s = check_device_range(beta, lay.beta_bytes, "beta")) != SQN_OK)
+        return s;
+    void* scr = nullptr;
+    if ((s = scratch_address(device, &scr)) != SQN_OK)
+        return s;
+
+    // live mask, row distances and capped distances of one plane at a time;
+    // every kernel of the preparation writes its whole array before it is
+    // read, so nothing needs clearing
+    sqn::PrepareWork pw;
+    memset(&pw, 0, sizeof(pw));
+    uint8_t* w = static_cast<uint8_t*>(scr);
+    pw.live = w;
+    pw.f = reinterpret_cast<uint16_t*>(w + align256(texels));
+    pw.dist = reinterpret_cast<uint16_t*>(w + align256(texels) + align256(texels * sizeof(uint16_t)));
+    char* base = static_cast<char*>(caches->block);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = hipSuccess;
+    for (int j = 0; j < 3 && e == hipSuccess; ++j)
+        e = sqn::prepare_sigma_plane(sigma_planes[j], desc->sigma_dtype, desc->n_p, base + lay.off_sigma[j], pw, st);
+    for (int j = 0; j < 3 && e == hipSuccess; ++j)
+        e = hipMemcpyAsync(base + lay.off_uvw[j], uvw_planes[j], lay.uvw_bytes, hipMemcpyDeviceToDevice, st);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(base + lay.off_beta, beta, lay.beta_bytes, hipMemcpyDeviceToDevice, st);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(SQN_ERR_DEVICE, "cache preparation failed (the handle's contents are now unspecified): %s",
+                    hipGetErrorString(e));
+    }
+    // later renders with the handle read the new arrays
+    caches->desc = *desc;
+    for (int j = 0; j < 3; ++j) {
+        caches->sigma[j] = base + lay.off_sigma[j];
+        caches->uvw[j] = base + lay.off_uvw[j];
+    }
+    caches->beta = base + lay.off_beta;
+    for (int r = 0; r < 3; ++r)
+        caches->scale[r] = static_cast<float>(desc->n_p - 1) / (desc->bbox_max[r] - desc->bbox_min[r]);
+    caches->tau_eps = tau_threshold(desc->t_eps);
+    clear_error();
+    return SQN_OK;
+}
+
 sqn_status sqn_create_networks(const sqn_mlp_desc pos[3], const sqn_mlp_desc* dir, int32_t D,
                                int32_t pos_freq, int32_t dir_freq, void* stream, sqn_networks** out)
 {
@@ -730,7 +876,7 @@ sqn_status sqn_create_networks(const sqn_mlp_desc pos[3], const sqn_mlp_desc* di
     h->pos_in = pos_in;
     h->dir_in = dir_in;
     *out = h;
-    g_last_error.clear();
+    clear_error();
     return SQN_OK;
 }
 
@@ -887,6 +1033,6 @@ const char* sqn_status_string(sqn_status status)
     return "unknown status";
 }
 
-const char* sqn_last_error(void) { return g_last_error.c_str(); }
+const char* sqn_last_error(void) { return g_last_error; }
 
 }  // extern "C"
