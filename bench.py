@@ -29,6 +29,7 @@ HBM_PEAK_GBS = 8000.0
 WORKLOAD_TEXT = {
     "tiny": "64x64 image, 64 uniform samples/ray, k=64 D=8 fp32 caches, 32x32 fp32 direction cache, 16 blobs",
     "paper": "800x800 image, 192 uniform samples/ray, k=256 D=8 fp16 caches, 128x128 fp16 direction cache, 64 blobs sigma_max 50",
+    "paper512": "800x800 image, 256 uniform samples/ray, the paper's 512 cache (k=512, sigma fp32, uvw fp16, D=8), 64x64 fp16 direction cache, 64 blobs sigma_max 50",
     "large": "800x800 image, 192 uniform samples/ray, k=1024 D=8 fp16 caches, 384x384 fp16 direction cache, 64 blobs sigma_max 200",
     "batch": "100 spiral views of 800x800, 192 uniform samples/ray, k=256 D=8 fp16 caches, 128x128 fp16 direction cache",
     "stress": "1920x1080 image, 384 stratified samples/ray, k=2048 D=16 fp16 caches, 512x512 fp16 direction cache, 256 blobs",
@@ -52,11 +53,20 @@ def algorithmic_bytes(cfg, n_rays, live_inbox, occupied):
     return n_rays * per_ray + live_inbox * 3 * b_sigma + occupied * 3 * 3 * cfg.D * b
 
 
-def measured_traffic(config_name, kind="render"):
-    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE /
-    WRITE_SIZE passes (profiles/<kind>_traffic_<workload>.json), scaled by
-    the counters of kernels of known traffic; None when no such file exists
-    or the kernel source has changed since the counters were taken."""
+# Cycles per second of the vector-memory data path (TD) over all CUs:
+# 256 CUs x 2.4 GHz.  Access-pattern probes on this GPU keep TD busy on every
+# cycle, and each gather's busy cycles match its cost there.
+TD_PEAK_GCYCLES = 256 * 2.4
+CLOCK_GHZ = 2.4
+
+
+def counter_record(config_name, kind="render"):
+    """The committed rocprofv3 counter record of a workload's kernel
+    (profiles/<kind>_traffic_<workload>.json): HBM bytes per launch from the
+    FETCH_SIZE / WRITE_SIZE passes scaled by kernels of known traffic, and
+    for render kernels the TD busy cycles, L1 accesses and VALU
+    instructions per launch.  None when no such file exists or the kernel
+    source has changed since the counters were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"{kind}_traffic_{config_name}.json")
     src = os.path.join(ROOT, "paper_2204_02585_amd", "csrc", f"{kind}.hip")
@@ -67,7 +77,42 @@ def measured_traffic(config_name, kind="render"):
         return None
     if rec.get(f"{kind}_hip_sha256_16") != sha:
         return None
-    return int(rec["traffic_bytes_per_launch"])
+    return rec
+
+
+def measured_traffic(config_name, kind="render"):
+    rec = counter_record(config_name, kind)
+    return None if rec is None else int(rec["traffic_bytes_per_launch"])
+
+
+def render_roofline(rec, ms, bytes_alg):
+    """Roofline of the render kernel against the unit its counters show
+    busiest, the vector-memory data path (TD): achieved = TD busy CU-cycles
+    per launch (committed counters of this kernel) over the launch time
+    measured here, so frac is the fraction of the launch the data path is
+    busy.  VALU issue per CU per clock from the same counters; the method's
+    algorithmic bytes per launch (sigma^j of every live in-box sample, three
+    uvw records per occupied one, beta corners and outputs per ray) as the
+    rate the kernel serves them; HBM bytes from the FETCH/WRITE counters
+    against the 8 TB/s HBM peak."""
+    sec = ms * 1e-3
+    td = None if rec is None else rec.get("td_busy_cycles_per_launch")
+    achieved = None if td is None else td / sec / 1e9
+    traffic = None if rec is None else int(rec["traffic_bytes_per_launch"])
+    valu = None if rec is None else rec.get("valu_insts_per_launch")
+    return {"bound": "vmem", "achieved": None if achieved is None else round(achieved, 2),
+            "peak": round(TD_PEAK_GCYCLES, 1), "unit": "G busy cycles/s of the TD data path, all CUs",
+            "frac": None if achieved is None else round(achieved / TD_PEAK_GCYCLES, 4),
+            "traffic": traffic,
+            "basis": "rocprofv3 TD_TD_BUSY_sum of this kernel per launch (profiles/) / launch time measured "
+                     "here; peak = 256 CUs x 2.4 GHz",
+            "td_busy_cycles_per_launch": None if td is None else int(td),
+            "valu_insts_per_cu_clock": None if valu is None else round(valu / (256 * CLOCK_GHZ * 1e9 * sec), 3),
+            "served_algorithmic_gbs": round(bytes_alg / sec / 1e9, 1),
+            "algorithmic_bytes_per_launch": int(bytes_alg),
+            "hbm_gbs": None if traffic is None else round(traffic / sec / 1e9, 1),
+            "hbm_frac": None if traffic is None else round(traffic / sec / 1e9 / HBM_PEAK_GBS, 4),
+            "kernel_ms_per_launch": round(ms, 5)}
 
 
 # Worker threads a process on a one-GPU share of the shared host may use.
@@ -431,12 +476,8 @@ def main():
                     "empty_fraction_of_live_inbox": round(1.0 - occupied / live_inbox, 4) if live_inbox else None,
                     "live_inbox_msamples_per_s": round(live_inbox / (ms * 1e-3) / 1e6, 1),
                     "occupied_msamples_per_s": round(occupied / (ms * 1e-3) / 1e6, 1)},
-        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                     "traffic": (measured_traffic(cfg.name)
-                                 if args.lanes == 0 and not args.dense else None),
-                     "algorithmic_bytes_per_launch": int(bytes_alg),
-                     "kernel_ms_per_launch": round(ms, 5)},
+        "roofline": render_roofline(counter_record(cfg.name) if args.lanes == 0 and not args.dense else None,
+                                    ms, bytes_alg),
         "cpu_baseline": base,
         "ceilings": ceilings,
         "wall_s_timed": round(wall, 4),

@@ -26,6 +26,7 @@
 // fused multiply-adds explicitly.
 #include <math.h>
 
+#include "atan2_lookup.h"
 #include "sqn_internal.h"
 
 namespace sqn {
@@ -319,40 +320,6 @@ __device__ __forceinline__ void clip_to_box(const RenderParams& P, const float o
 
 // ---------------------------------------------------------------------------
 // value path
-
-// atan2 in binary64 to within 2e-14 (checked against the library atan2 on
-// 2 x 10^5 random pairs and the signed-zero cases): octant reduction to
-// t = min/max, then t > tan(pi/8) to (t - 1)/(t + 1) in one division, and an
-// odd polynomial t + t^3 P(t^2) with P a least-squares fit of
-// (atan(t) - t)/t^3 at Chebyshev nodes of [0, tan^2(pi/8)].  Signs and
-// zeros follow atan2.  The direction lookup needs the angles to about 1e-8.
-__device__ __forceinline__ double atan2_lookup(double y, double x)
-{
-    constexpr double kTanPi8 = 0.41421356237309503;
-    const double ax = fabs(x), ay = fabs(y);
-    const double mx = fmax(ax, ay), mn = fmin(ax, ay);
-    const bool big = mn > kTanPi8 * mx;
-    const double num = big ? mn - mx : mn;
-    const double den = big ? mn + mx : mx;
-    const double t = den > 0.0 ? num / den : 0.0;
-    const double s = t * t;
-    double p = 0.03139479947774411;
-    p = fma(p, s, -0.05926635751528511);
-    p = fma(p, s, 0.0757883898701557);
-    p = fma(p, s, -0.09080691227325184);
-    p = fma(p, s, 0.11110579634656349);
-    p = fma(p, s, -0.14285699429416587);
-    p = fma(p, s, 0.1999999981132898);
-    p = fma(p, s, -0.333333333326259);
-    double r = fma(t * s, p, t);
-    if (big)
-        r += 0.25 * kPi;
-    if (ay > ax)
-        r = 0.5 * kPi - r;
-    if (signbit(x))
-        r = kPi - r;
-    return copysign(r, y);
-}
 
 // Bilinear lookup of beta (Sec. 3.4), once per ray by one lane.  The angles
 // and grid coordinates are computed in binary64 (theta = polar angle from +z

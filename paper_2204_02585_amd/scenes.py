@@ -105,6 +105,11 @@ CONFIGS = {
     # a small forward-facing case the oracle renders in full
     "llff_tiny": Config("llff_tiny", 10, 48, 36, 64, 64, 8, 16, 16, "f32", 48, 50.0, 0.05, 0.25,
                         focal=0.8 * 48, forward=True),
+    # the paper's own shape for its 800x800 timings: 256 samples per ray and
+    # the 512 cache with its precisions (sigma fp32, uvw and beta fp16,
+    # n_d = 64, D = 8), blobs as "paper"
+    "paper512": Config("paper512", 11, 800, 800, 256, 512, 8, 64, 64, "f16", 64, 50.0, 0.1, 0.4,
+                       sigma_dtype="f32"),
     # the alt decoder at the paper's alt cache size (n_p = 512, n_d = 256)
     "alt512": Config("alt512", 7, 800, 800, 192, 512, 8, 256, 256, "f16", 64, 50.0, 0.1, 0.4,
                      sigma_channels=12),

@@ -5,6 +5,12 @@ import numpy as np
 # value tolerances: binary32 caches 1e-5 absolute, binary16 caches 1e-3
 # absolute (the oracle reads the same binary16 values)
 ATOL = {"f32": 1e-5, "f16": 1e-3}
+# regression bound asserted beside them: the oracle reads the very binary16
+# values the kernel reads, so both sides evaluate the same real numbers and
+# only the kernel's binary32 value path (binary64 sums) separates them,
+# bounded near 1e-6 whatever the cache dtype; 1e-5 flags a value-path
+# regression that the 1e-3 criterion of binary16 caches would let through
+REGRESSION_ATOL = 1e-5
 
 
 def scene_atol(scene):
@@ -58,6 +64,7 @@ def compare(gpu, ref, ids, atol, label=""):
     print(f"[parity {label}] rays={len(ids)} max|drgb|={e_rgb:.3g} max|ddepth|={e_dep:.3g}", flush=True)
     assert e_rgb <= atol, (label, e_rgb)
     assert e_dep <= atol, (label, e_dep)
+    assert e_rgb <= REGRESSION_ATOL and e_dep <= REGRESSION_ATOL, (label, "regression bound", e_rgb, e_dep)
     if st is not None:
         s = st[ids]
         for k, name in enumerate(("stop", "n_inbox", "n_occ", "hash")):

@@ -236,7 +236,7 @@ def test_large_ragged_two_views():
 # ------------------------------------------------------- full workload sizes
 
 @pytest.mark.parametrize("mode", MODES)
-@pytest.mark.parametrize("name,n_random", [("paper", 40000), ("large", 40000)])
+@pytest.mark.parametrize("name,n_random", [("paper", 40000), ("large", 40000), ("paper512", 30000)])
 def test_full_size_single_view(name, n_random, mode):
     sc = scenes.make_scene(name)
     cfg = sc.config
