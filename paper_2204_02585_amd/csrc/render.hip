@@ -586,6 +586,53 @@ __device__ __forceinline__ uint32_t fnv1a_word(uint32_t h, uint32_t x)
     return h;
 }
 
+// Deferred colour.  An occupied live sample needs its three uvw records
+// (nine 16-byte loads at D = 8, binary16) and 3 x 3D multiply-adds; issued
+// where the sample is found, they run with only the wave's occupied lanes
+// active, and a 16-byte gather costs the memory pipeline the same however few
+// lanes take part.  Instead the sample's texels, its Eq. 1 weight
+// w = T (1 - exp(-sigma delta)) and its ray go to a per-wave ring of kQueue
+// entries in LDS, and whenever 64 are waiting the whole wave evaluates them,
+// one per lane, adding w c into per-ray binary64 sums in LDS (the colour
+// sums are independent of the order of the samples up to binary64
+// rounding).  Depth, sum w t, needs no records and stays in registers.
+constexpr uint32_t kQueue = 128;   // 63 waiting + 64 pushed at most
+
+constexpr bool defers_colour(int DC, bool LIN) { return !LIN && DC == 8; }
+
+struct ColourQueue {
+    uint4* entries;        // [kQueue] wave-private ring: texel0 | slot << 26, texel1, texel2, w
+    double* acc;           // [rays per wave][3] rgb sums of the wave's rays
+    const float* beta;     // beta of ray slot 0 of the wave; slot r, component k at beta[r + k * BS]
+};
+
+// Evaluate the n oldest entries with every lane of the wave present here.
+template <typename UT, int DC, bool LIN, int BS>  // Eq. 4 only (LIN false)
+__device__ __forceinline__ void drain_colour(const RenderParams& P, const ColourQueue& cq, uint32_t& head,
+                                             uint32_t n)
+{
+    const uint64_t ex = __builtin_amdgcn_read_exec();
+    const uint32_t workers = static_cast<uint32_t>(__builtin_popcountll(ex));
+    const uint32_t rank = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(ex >> 32),
+                                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(ex), 0u));
+    for (uint32_t done = 0; done < n; done += workers) {
+        const uint32_t k = done + rank;
+        if (k < n) {
+            const uint4 e = cq.entries[(head + k) & (kQueue - 1)];
+            const uint32_t slot = e.x >> 26;
+            const uint32_t t0 = e.x & ((1u << 26) - 1u);
+            float col[3];
+            sample_colour<UT, DC, BS>(P, t0, e.y, e.z, cq.beta + slot, col);
+            const double w = static_cast<double>(__uint_as_float(e.w));
+            double* a = cq.acc + 3 * slot;
+            atomicAdd(a + 0, w * static_cast<double>(col[0]));
+            atomicAdd(a + 1, w * static_cast<double>(col[1]));
+            atomicAdd(a + 2, w * static_cast<double>(col[2]));
+        }
+    }
+    head = (head + n) & (kQueue - 1);
+}
+
 #ifndef SQN_XCD_BLOCK
 #define SQN_XCD_BLOCK 4
 #endif
@@ -802,7 +849,7 @@ template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool L
           int BS = kBlockThreads>
 __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, int32_t u,
                                            int32_t v, int32_t lane, float* const beta, float* const lin,
-                                           const RayGeom* pre = nullptr)
+                                           const ColourQueue& cq, int32_t slot, const RayGeom* pre = nullptr)
 {
     static_assert(L == 1 || L == 4 || L == 8, "one, four or eight lanes per ray");
     const int32_t s = (L == 1) ? 0 : (lane & (L - 1));
@@ -853,15 +900,39 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
     const float leap_margin = geo.margin;
     const int32_t n_p = P.n_p;
     const float hi_node = static_cast<float>(n_p - 1);
+    // Eq. 4 at D = 8 defers colour to the wave's queue (measured: 4-8%
+    // faster on every D = 8 workload; 10% slower on the HBM-bound D = 16
+    // one); Eq. 5 keeps a row of folded weights per ray in LDS and, like the
+    // other D, evaluates colour where the sample is found
+    constexpr bool kDefer = defers_colour(DC, LIN);
     uint64_t tau = 0;              // optical depth before the chunk, 2^-32 units
     double acc_r = 0.0, acc_g = 0.0, acc_b = 0.0, acc_t = 0.0;
     int32_t last_live = -1;
     uint32_t n_inbox = 0, n_occ = 0, hash = 2166136261u;
+    // the ray's colour sums, written by whichever lanes evaluate its samples
+    if (kDefer && s == 0) {
+        cq.acc[3 * slot + 0] = 0.0;
+        cq.acc[3 * slot + 1] = 0.0;
+        cq.acc[3 * slot + 2] = 0.0;
+    }
+    uint32_t q_head = 0, q_count = 0;   // the wave's queue, wave-uniform
 
     int32_t base = i0;
     // t of this lane's sample in the current chunk
     float t = (base <= i1) ? sample_t(P, stratified, ray_key, base + s) : 0.0f;
-    while (base <= i1 && tau <= static_cast<uint64_t>(P.tau_eps)) {
+    // with deferred colour every lane present stays in the loop until the
+    // wave is done, so that the whole wave evaluates the queued colours;
+    // otherwise a lane leaves as soon as its ray is done
+    for (;;) {
+        const bool active = base <= i1 && tau <= static_cast<uint64_t>(P.tau_eps);
+        if constexpr (kDefer) {
+            if (__builtin_amdgcn_ballot_w64(active) == 0)
+                break;
+        } else if (!active) {
+            break;
+        }
+        bool pushed = false;
+        if (active) {
         const int32_t i = base + s;
         const bool in_range = i <= i1;
         const float t_next_chunk = sample_t(P, stratified, ray_key, base + L + s);
@@ -936,6 +1007,7 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
             }
             return n;
         };
+        bool leapt = false;
         if constexpr (SKIP && L == 1) {
             if (leap != 0) {
                 // samples i .. leap-1 are empty: sample i has sigma^j = 0 in
@@ -945,9 +1017,10 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
                     n_inbox += count_inbox(i, leap);
                 base = leap;
                 t = sample_t(P, stratified, ray_key, base);
-                continue;
+                leapt = true;
             }
         }
+        if (!leapt) {
         float q = 0.0f;
         uint64_t excl = 0, total = 0;
         // a chunk in which no lane of the wave is occupied adds nothing to
@@ -975,7 +1048,9 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
         // tau_i = tau <= tau_eps and i <= i1
         const bool live = (L == 1) || (in_range & (tau_i <= static_cast<uint64_t>(P.tau_eps)));
         const bool occ = live & (sigma > 0.0f);
-        if (occ) {
+        // queue positions of this step's occupied samples, in lane order
+        const uint64_t occ_mask = kDefer ? __builtin_amdgcn_ballot_w64(occ) : 0;
+        if (occ && !kDefer) {
             float col[3];
             if constexpr (LIN)
                 sample_colour_lin<UT, DC>(P, __umul24(ix, n_p) + iy, __umul24(iy, n_p) + iz,
@@ -990,6 +1065,18 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
             acc_g = fma(w, static_cast<double>(col[1]), acc_g);
             acc_b = fma(w, static_cast<double>(col[2]), acc_b);
             acc_t = fma(w, static_cast<double>(t), acc_t);
+        }
+        if (occ && kDefer) {
+            const float T = transmittance(tau_i);
+            const float alpha = -expm1f(-q);
+            const float w = T * alpha;
+            acc_t = fma(static_cast<double>(w), static_cast<double>(t), acc_t);
+            const uint32_t rank = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(occ_mask >> 32),
+                                                            __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(occ_mask), 0u));
+            cq.entries[(q_head + q_count + rank) & (kQueue - 1)] =
+                make_uint4((__umul24(ix, n_p) + iy) | (static_cast<uint32_t>(slot) << 26), __umul24(iy, n_p) + iz,
+                           __umul24(iz, n_p) + ix, __float_as_uint(w));
+            pushed = true;
         }
         if (L > 1 && live)
             last_live = i;
@@ -1029,12 +1116,26 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
         }
         t = (next == base + L) ? t_next_chunk : sample_t(P, stratified, ray_key, next + s);
         base = next;
+        }   // !leapt
+        }   // active
+        if constexpr (kDefer) {
+            // whole wave: count the pushes; evaluate 64 once they are waiting
+            q_count += static_cast<uint32_t>(__builtin_popcountll(__builtin_amdgcn_ballot_w64(pushed)));
+            if (q_count >= 64) {
+                drain_colour<UT, DC, LIN, BS>(P, cq, q_head, 64);
+                q_count -= 64;
+            }
+        }
     }
+    if constexpr (kDefer)
+        drain_colour<UT, DC, LIN, BS>(P, cq, q_head, q_count);
 
     // combine the lanes of the ray
-    acc_r = grp_sum<L>(acc_r);
-    acc_g = grp_sum<L>(acc_g);
-    acc_b = grp_sum<L>(acc_b);
+    if constexpr (!kDefer) {
+        acc_r = grp_sum<L>(acc_r);
+        acc_g = grp_sum<L>(acc_g);
+        acc_b = grp_sum<L>(acc_b);
+    }
     acc_t = grp_sum<L>(acc_t);
     // the first non-live sample: with one lane per ray the loop leaves as
     // soon as the optical depth crosses, at the index after the last sample
@@ -1050,6 +1151,11 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
     // the partially written lines of a pixel tile from being allocated in
     // L2 and written back piecemeal while the gathers churn it
     if (P.rgb) {
+        if constexpr (kDefer) {
+            acc_r = cq.acc[3 * slot + 0];
+            acc_g = cq.acc[3 * slot + 1];
+            acc_b = cq.acc[3 * slot + 2];
+        }
         __builtin_nontemporal_store(static_cast<float>(acc_r), P.rgb + 3 * ray + 0);
         __builtin_nontemporal_store(static_cast<float>(acc_g), P.rgb + 3 * ray + 1);
         __builtin_nontemporal_store(static_cast<float>(acc_b), P.rgb + 3 * ray + 2);
@@ -1099,7 +1205,8 @@ constexpr int occupancy()
     constexpr int rec0 = waves_per_simd(3 * DC * static_cast<int>(sizeof(UT)));
     constexpr int rec = (NDC || (L >= 4 && !LIN)) && rec0 > 4 ? rec0 - 1 : rec0;
     constexpr int regs = LIN && rec > 6 ? 6 : rec;
-    constexpr int lds = 4 * (lin_smem_floats<DC, LIN>() + beta_smem_floats<DC, LIN>());
+    constexpr int lds = 4 * (lin_smem_floats<DC, LIN>() + beta_smem_floats<DC, LIN>())
+                        + (defers_colour(DC, LIN) ? 4 * static_cast<int>(kQueue) * 16 + 4 * (64 / L) * 3 * 8 : 0);
     constexpr int by_lds = 163840 / lds;
     return regs < by_lds ? regs : (by_lds < 1 ? 1 : by_lds);
 }
@@ -1114,6 +1221,10 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) 
     // Eq. 5: one row of folded weights per ray, written and read only by
     // the ray's own lanes
     __shared__ __align__(16) float lin_smem[lin_smem_floats<DC, LIN>()];
+    // deferred colour: a ring of queued samples and the rays' rgb sums per wave
+    constexpr bool kDefer = defers_colour(DC, LIN);
+    __shared__ uint4 queue_smem[kDefer ? 4 * kQueue : 1];
+    __shared__ double qacc_smem[kDefer ? 4 * (64 / L) * 3 : 1];
     const int32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int32_t tile = xcd_tile_order(static_cast<int32_t>(blockIdx.x), P.n_groups);
     const int32_t tiles_per_view = P.tiles_x * P.tiles_y;
@@ -1156,19 +1267,23 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) 
         }
         __syncthreads();
         const int32_t r = wave * RPW + slot;
+        ColourQueue cq;
+        cq.entries = queue_smem + wave * kQueue;
+        cq.acc = qacc_smem + wave * RPW * 3;
+        cq.beta = beta_smem + wave * RPW;
         if (view < P.n_views && u < P.width && v < P.height)
             render_ray<ST, UT, DC, STATS, L, SKIP, LIN, NDC, true, 64>(P, view, u, v, lane, beta_smem + r,
-                                                                      LIN ? lin_row(r) : nullptr, &geom[r]);
+                                                                      LIN ? lin_row(r) : nullptr, cq, slot, &geom[r]);
     } else {
         // all lanes of a ray agree on this, so a lane group is never split
+        static_assert(!LIN, "the Eq. 5 decoder runs with four lanes per ray");
         if (view < P.n_views && u < P.width && v < P.height) {
-            float* lin = nullptr;
-            if constexpr (LIN) {
-                constexpr int32_t stride = DC > 0 ? lin_stride(DC) : 0;
-                lin = lin_smem + (threadIdx.x / 4) * (DC > 0 ? stride : P.lin_stride);
-            }
-            render_ray<ST, UT, DC, STATS, L, SKIP, LIN, NDC>(P, view, u, v, lane,
-                                                        LIN ? beta_smem : beta_smem + threadIdx.x, lin);
+            ColourQueue cq;
+            cq.entries = queue_smem + wave * kQueue;
+            cq.acc = qacc_smem + wave * 64 * 3;
+            cq.beta = beta_smem + wave * 64;
+            render_ray<ST, UT, DC, STATS, L, SKIP, LIN, NDC>(P, view, u, v, lane, beta_smem + threadIdx.x, nullptr,
+                                                        cq, slot);
         }
     }
 }
