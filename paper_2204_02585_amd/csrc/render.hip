@@ -209,6 +209,16 @@ __device__ __forceinline__ uint32_t nearest_node(float p, float lo, float scale,
     return static_cast<uint32_t>(floor_to_int(__builtin_amdgcn_fmed3f(h, 0.0f, hi_node)));
 }
 
+// nearest_node for a sample inside the box, where 1/2 <= g + 1/2 <= n_p - 1/2
+// (bmin <= p <= bmax, and binary32 subtraction and multiplication are
+// monotone), so the clamp would change nothing.
+__device__ __forceinline__ uint32_t nearest_node_inside(float p, float lo, float scale)
+{
+    const float g = (p - lo) * scale;
+    const float h = g + 0.5f;
+    return static_cast<uint32_t>(floor_to_int(h));
+}
+
 // trunc(min(q, 2^16) * 2^32) for q >= 0: the integer part and the (exactly
 // representable) fraction convert separately.
 __device__ __forceinline__ uint64_t fixed_q(float q)
@@ -285,11 +295,16 @@ __device__ __forceinline__ bool ndc_ray(const RenderParams& P, float o[3], float
 // position o + t d and of this estimate), then by two samples.  An axis with
 // a (nearly) zero direction component constrains nothing here unless the
 // component is exactly zero, where p = o holds exactly.
-__device__ __forceinline__ void clip_to_box(const RenderParams& P, const float o[3],
-                                            const float d[3], int32_t& i0, int32_t& i1)
+// [j0, j1] is the range of samples certainly inside: the crossings narrowed
+// by the same margin and one more sample on each side, so every such sample
+// passes the six exact box tests (its binary32 position is within a few ulp
+// of the exact one, the margin is 160 times that) and needs no clamp of its
+// node indices; empty when an axis has a tiny nonzero component.
+__device__ __forceinline__ void clip_to_box(const RenderParams& P, const float o[3], const float d[3],
+                                            int32_t& i0, int32_t& i1, int32_t& j0, int32_t& j1)
 {
-    float lo = -INFINITY, hi = INFINITY;
-    bool empty = false;
+    float lo = -INFINITY, hi = INFINITY, lo_in = -INFINITY, hi_in = INFINITY;
+    bool empty = false, no_inner = false;
 #pragma unroll
     for (int r = 0; r < 3; ++r) {
         if (d[r] == 0.0f) {
@@ -303,6 +318,10 @@ __device__ __forceinline__ void clip_to_box(const RenderParams& P, const float o
             const float m = 1e-5f * (fmaxf(fabsf(tmin), fabsf(tmax)) + (fabsf(o[r]) + bmag) * fabsf(inv));
             lo = fmaxf(lo, tmin - m);
             hi = fminf(hi, tmax + m);
+            lo_in = fmaxf(lo_in, tmin + m);
+            hi_in = fminf(hi_in, tmax - m);
+        } else {
+            no_inner = true;
         }
     }
     const float n_last = static_cast<float>(P.n_samples - 1);
@@ -316,6 +335,17 @@ __device__ __forceinline__ void clip_to_box(const RenderParams& P, const float o
     }
     i0 = static_cast<int32_t>(f0);
     i1 = static_cast<int32_t>(f1);
+    float g0 = ceilf((lo_in - P.near_t) * P.inv_dt) + 1.0f;
+    float g1 = floorf((hi_in - P.near_t) * P.inv_dt) - 1.0f;
+    // inside [i0, i1]; a NaN or an infinite bound gives the empty range
+    g0 = fminf(fmaxf(g0, f0), n_last + 1.0f);
+    g1 = fminf(fmaxf(g1, -1.0f), f1);
+    if (empty || no_inner || !(lo_in <= hi_in) || !(g0 <= g1)) {
+        g0 = 1.0f;
+        g1 = 0.0f;
+    }
+    j0 = static_cast<int32_t>(g0);
+    j1 = static_cast<int32_t>(g1);
 }
 
 // ---------------------------------------------------------------------------
@@ -772,7 +802,8 @@ struct RayGeom {
     float dn;
     float g0[3], inv_ds[3];   // grid coordinate g = g0 + t ds per axis, 1/ds
     float margin;             // texels a leap keeps from its square's edge
-    int32_t i0, i1;
+    int32_t i0, i1;           // samples that may lie in the box
+    int32_t j0, j1;           // samples certainly in the box
 };
 
 // World ray through the pixel centre of (u, v) (camera looks down -z).
@@ -811,11 +842,13 @@ __device__ __forceinline__ void march_geometry(const RenderParams& P, const floa
         no_samples = !ndc_ray(P, g.o, g.d);
     const float d00 = g.d[0] * g.d[0], d11 = g.d[1] * g.d[1], d22 = g.d[2] * g.d[2];
     g.dn = sqrtf((d00 + d11) + d22);
-    clip_to_box(P, g.o, g.d, g.i0, g.i1);
+    clip_to_box(P, g.o, g.d, g.i0, g.i1, g.j0, g.j1);
     if constexpr (NDC) {
         if (no_samples) {
             g.i0 = 1;
             g.i1 = 0;
+            g.j0 = 1;
+            g.j1 = 0;
         }
     }
     g.margin = 0.0f;
@@ -894,7 +927,7 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
     const float* const o = geo.o;
     const float* const d = geo.d;
     const float dn = geo.dn;
-    const int32_t i0 = geo.i0, i1 = geo.i1;
+    const int32_t i0 = geo.i0, i1 = geo.i1, j0 = geo.j0, j1 = geo.j1;
     const float* const g0 = geo.g0;
     const float* const inv_ds = geo.inv_ds;
     const float leap_margin = geo.margin;
@@ -943,14 +976,27 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
             const float td = t * d[r];
             p[r] = o[r] + td;
         }
-        const bool inside = in_range & (p[0] >= P.bmin[0]) & (p[0] <= P.bmax[0]) & (p[1] >= P.bmin[1])
-                            & (p[1] <= P.bmax[1]) & (p[2] >= P.bmin[2]) & (p[2] <= P.bmax[2]);
+        bool inside;
+        uint32_t ix, iy, iz;
+        // when every lane's sample is certainly in the box the six exact
+        // tests would all pass and the node indices need no clamp (a
+        // wave-uniform branch)
+        const bool deep = (i >= j0) & (i <= j1);
+        if (__builtin_amdgcn_ballot_w64(deep) == __builtin_amdgcn_read_exec()) {
+            inside = true;
+            ix = nearest_node_inside(p[0], P.bmin[0], P.scale[0]);
+            iy = nearest_node_inside(p[1], P.bmin[1], P.scale[1]);
+            iz = nearest_node_inside(p[2], P.bmin[2], P.scale[2]);
+        } else {
+            inside = in_range & (p[0] >= P.bmin[0]) & (p[0] <= P.bmax[0]) & (p[1] >= P.bmin[1])
+                     & (p[1] <= P.bmax[1]) & (p[2] >= P.bmin[2]) & (p[2] <= P.bmax[2]);
+            // node indices are clamped to the grid for any position; they
+            // are used only for samples inside the box
+            ix = nearest_node(p[0], P.bmin[0], P.scale[0], hi_node);
+            iy = nearest_node(p[1], P.bmin[1], P.scale[1], hi_node);
+            iz = nearest_node(p[2], P.bmin[2], P.scale[2], hi_node);
+        }
         float sigma = 0.0f;
-        // node indices are clamped to the grid for any position; they are
-        // used only for samples inside the box
-        const uint32_t ix = nearest_node(p[0], P.bmin[0], P.scale[0], hi_node);
-        const uint32_t iy = nearest_node(p[1], P.bmin[1], P.scale[1], hi_node);
-        const uint32_t iz = nearest_node(p[2], P.bmin[2], P.scale[2], hi_node);
         int32_t leap = 0;
         if (inside) {
             // Eq. 5: a sample in an empty cell of the 3-D cell grid has
