@@ -281,7 +281,12 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
     p.tau_eps = h->tau_eps;
     p.seed = h->desc.seed;
     p.inv_dt = 1.0f / p.dt;
-    p.leap_slack = static_cast<float>(ldexp(fabs(static_cast<double>(near_plane)) * p.inv_dt, -19));
+    {
+        const double k = (1.0 - ldexp(1.0, -19)) / static_cast<double>(p.dt);
+        p.leap_k = static_cast<float>(k);
+        p.leap_c = static_cast<float>(static_cast<double>(near_plane) * k
+                                      + ldexp(fabs(static_cast<double>(near_plane)) / static_cast<double>(p.dt), -19));
+    }
     const int64_t rays = static_cast<int64_t>(n_poses) * in->width * in->height;
     p.skip = h->skip;
     // the folded Eq. 5 weights are shared by the lanes of a ray in LDS, which

@@ -698,15 +698,17 @@ struct SigmaRecord<float> {
 
 // Sample index just past the exit parameter t_exit of a leap: every sample
 // below it has t_k <= t_exit.  x = (t_exit - near) / dt is pulled in by
-// 2^-19 (x + |near| / dt), more than the binary32 rounding of x and of
-// t_k = near + k dt together (under 8 units of 2^-24 of those magnitudes);
-// a stratified sample k lies at or below t_{k+1} of the uniform grid, so it
-// lands one index earlier.  Non-positive x gives an index <= 0 (the caller
-// clamps), +inf stays +inf, NaN stays NaN.
+// 2^-19 (x + |near| / dt): y = t_exit k - c in one fused multiply-add, with
+// k = (1 - 2^-19) / dt and c = near k + 2^-19 |near| / dt rounded from
+// binary64 on the host.  The roundings of k, c and the fused multiply-add
+// stay under 3 units of 2^-24 of |x| + |near| / dt, those of the binary32
+// t_k = near + k dt under 8 more, and the pull-in is 32 units; a stratified
+// sample k lies at or below t_{k+1} of the uniform grid, so it lands one
+// index earlier.  Non-positive y gives an index <= 0 (the caller clamps),
+// +inf stays +inf, NaN stays NaN.
 __device__ __forceinline__ float leap_index(const RenderParams& P, float t_exit)
 {
-    const float x = (t_exit - P.near_t) * P.inv_dt;
-    const float y = x * (1.0f - 0x1p-19f) - P.leap_slack;
+    const float y = fmaf(t_exit, P.leap_k, -P.leap_c);
     return floorf(y) + (P.stratified ? 0.0f : 1.0f);
 }
 

@@ -38,7 +38,8 @@ struct RenderParams {
     int64_t tau_eps;          // floor(-ln(eps) 2^32), INT64_MAX for eps = 0
     uint64_t seed;
     float inv_dt;             // 1 / dt (conservative box clip and leap indices)
-    float leap_slack;         // 2^-19 |near| / dt: leap indices are pulled in by it
+    float leap_k, leap_c;     // leap index fma(t_exit, leap_k, -leap_c): leap_k = (1 - 2^-19) / dt,
+                              // leap_c = near leap_k + 2^-19 |near| / dt (binary64, rounded once)
     // launch geometry
     int32_t lanes;            // lanes per ray: 1, 4 or 8
     int32_t skip;             // 1: one lane per ray with empty-space leaps
