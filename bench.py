@@ -207,6 +207,33 @@ def memory_ceilings(cache_bytes):
     return out
 
 
+# lane patterns of the render kernel's loads: the sigma gathers are dword
+# loads with every lane in its own 64-byte segment (a quad holds four
+# samples of one ray, texels apart), the colour records 16-byte loads
+VMEM_PATTERNS = (("dword_lane_per_segment", 0, 0), ("dword_quad_per_segment", 0, 1),
+                 ("dwordx4_lane_per_segment", 1, 0), ("dwordx4_quad_per_segment", 1, 1))
+
+
+def vmem_ceiling():
+    """Cycles per wave-level load instruction on one CU with the
+    vector-memory data path saturated by gathers that the vector L1 serves
+    (libsqn_probe.so), for dword and 16-byte loads with every lane in its own
+    64-byte segment or a quad sharing one: what a load costs the path that
+    the render kernel's TD-busy fraction measures."""
+    import ctypes
+    from paper_2204_02585_amd import build as _build
+    lib = ctypes.CDLL(_build.PROBE_PATH)
+    lib.sqn_probe_vmem.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_double,
+                                   ctypes.POINTER(ctypes.c_float)]
+    cyc = ctypes.c_float()
+    out = {}
+    for label, wide, quads in VMEM_PATTERNS:
+        if lib.sqn_probe_vmem(wide, quads, 256, CLOCK_GHZ, ctypes.byref(cyc)) != 0:
+            raise RuntimeError("vector-memory probe failed")
+        out[label] = round(cyc.value, 2)
+    return out
+
+
 def mfma_ceiling():
     """Dense binary16 matrix-core rate of this GPU at two waves per SIMD
     (independent 32x32x16 products, libsqn_probe.so), TFLOP/s."""
@@ -358,6 +385,8 @@ def main():
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the ceiling probes (memory levels; matrix cores for gen_*)")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--vmem-probe", action="store_true",
+                    help="only run the vector-memory saturation probe and print its cycles per load")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB device-to-device 3 times (a kernel "
                          "of known traffic for scaling hardware byte counters)")
@@ -367,6 +396,10 @@ def main():
         print("bench.py measures one GPU: the render path has no cross-GPU step; "
               "run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
+
+    if args.vmem_probe:
+        print(json.dumps({"vmem_cycles_per_wave_load": vmem_ceiling(), "clock_ghz": CLOCK_GHZ}), flush=True)
+        return
 
     if args.config in GEN_TEXT:
         bench_generate(args)
@@ -441,6 +474,7 @@ def main():
         ceilings = memory_ceilings(scene.cache_nbytes())
         g = ceilings["gather64_gbs"][ceilings.pop("cache_label")]
         ceilings["render_vs_gather64_at_cache_size"] = round(gbs / g, 4)
+        ceilings["vmem_cycles_per_wave_load"] = vmem_ceiling()
 
     base = None
     if not args.no_cpu_baseline:

@@ -2,7 +2,9 @@
 // for the render kernel, streaming reads of a buffer (a footprint that one
 // XCD's L2 holds, one that the MALL holds, one that only HBM holds) and
 // random gathers of 64-byte records over a buffer, the access pattern of the
-// cache lookups; for cache generation, the rate of independent
+// cache lookups; the vector-memory data path at saturation, with gathers
+// that the vector L1 serves in the lane patterns of the render kernel's
+// loads; for cache generation, the rate of independent
 // v_mfma_f32_32x32x16_f16 products at two waves per SIMD.  A measurement aid
 // for bench.py, built as its own library (libsqn_probe.so); the render
 // library does not use it.
@@ -61,6 +63,38 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const uint4* __restric
     for (; i < n_reads; i += stride) {
         const uint4 v = buf[piece(i)];
         acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    if (acc == 0x9e3779b9u)
+        sink[threadIdx.x] = acc;
+}
+
+// Gathers from a 16 KiB buffer (256 segments of 64 bytes) that stays in
+// every CU's vector L1, four independent loads per lane and iteration, so
+// the memory data path is all that limits the rate.  A load's segment is a
+// hash of the lane (or, with `quads`, of the lane's quad: the four lanes of
+// a quad then share a segment) and of the load's number; within the
+// segment a lane reads dword (lane % 16) or, with 16-byte loads, piece
+// (lane % 4).  Every index stays below 4096 dwords / 1024 pieces.
+template <bool WIDE>
+__global__ __launch_bounds__(kThreads) void vmem_kernel(const uint32_t* __restrict__ buf, int iters, int quads,
+                                                        uint32_t* __restrict__ sink)
+{
+    const uint32_t lane = threadIdx.x & 63u;
+    const uint32_t who = quads ? (lane >> 2) : lane;
+    uint32_t h = (blockIdx.x * 0x9E3779B9u) ^ ((threadIdx.x >> 6) * 0x85EBCA6Bu) ^ (who * 0xC2B2AE35u);
+    uint32_t acc = 0;
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            h = h * 1664525u + 1013904223u;
+            const uint32_t seg = h >> 24;   // 0..255
+            if constexpr (WIDE) {
+                const uint4 v = reinterpret_cast<const uint4*>(buf)[seg * 4u + (lane & 3u)];
+                acc ^= v.x ^ v.y ^ v.z ^ v.w;
+            } else {
+                acc ^= buf[seg * 16u + (lane & 15u)];
+            }
+        }
     }
     if (acc == 0x9e3779b9u)
         sink[threadIdx.x] = acc;
@@ -181,6 +215,50 @@ int sqn_probe_gather(uint64_t bytes, uint64_t n_records, float* ms_out)
     (void)hipFree(sink);
     (void)hipFree(buf);
     return rc;
+}
+
+// Vector-memory data path at saturation: `iters` x 4 gathers per lane from
+// a 16 KiB L1-resident buffer, dword (wide = 0) or 16-byte (wide = 1)
+// loads, every lane its own 64-byte segment (quads = 0) or the four lanes of
+// a quad sharing one (quads = 1); 32 waves per CU.  *cycles_out is the
+// GPU time per wave-level load instruction on one CU, in cycles of
+// `clock_ghz`.  Returns 0, or 1 on a HIP error or bad argument.
+int sqn_probe_vmem(int wide, int quads, int iters, double clock_ghz, float* cycles_out)
+{
+    if (iters < 1 || clock_ghz <= 0.0 || !cycles_out || (wide != 0 && wide != 1) || (quads != 0 && quads != 1))
+        return 1;
+    int cus = 256;
+    int dev = 0;
+    if (hipGetDevice(&dev) == hipSuccess)
+        (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    constexpr uint64_t kBytes = 16384;
+    void* buf = nullptr;
+    uint32_t* sink = nullptr;
+    if (hipMalloc(&buf, kBytes) != hipSuccess)
+        return 1;
+    if (hipMalloc(reinterpret_cast<void**>(&sink), kThreads * 4) != hipSuccess) {
+        (void)hipFree(buf);
+        return 1;
+    }
+    int rc = hipMemset(buf, 1, kBytes) == hipSuccess ? 0 : 1;
+    const int blocks = cus * 8;
+    float ms = 0.0f;
+    if (rc == 0)
+        rc = time_launch(
+            [&] {
+                if (wide)
+                    vmem_kernel<true><<<blocks, kThreads>>>(static_cast<const uint32_t*>(buf), iters, quads, sink);
+                else
+                    vmem_kernel<false><<<blocks, kThreads>>>(static_cast<const uint32_t*>(buf), iters, quads, sink);
+            },
+            &ms);
+    (void)hipFree(sink);
+    (void)hipFree(buf);
+    if (rc != 0 || !(ms > 0.0f))
+        return 1;
+    const double insts_per_cu = static_cast<double>(blocks) * (kThreads / 64) * iters * 4 / cus;
+    *cycles_out = static_cast<float>(static_cast<double>(ms) * 1e-3 * clock_ghz * 1e9 / insts_per_cu);
+    return 0;
 }
 
 // Dense binary16 matrix-core rate: `iters` x 8 products of 32x32x16 per
