@@ -637,27 +637,70 @@ struct ColourQueue {
 };
 
 // Evaluate the n oldest entries with every lane of the wave present here.
-template <typename UT, int DC, bool LIN, int BS>  // Eq. 4 only (LIN false)
+// With all 64 lanes present a quad takes an entry: lane c < 3 evaluates
+// colour channel c, reading that channel's part of the entry's record in
+// each plane (16 bytes at D = 8 binary16), so the three loads of a quad fall
+// in the one or two 64-byte segments of a record instead of one segment per
+// lane, which is what a gather costs the memory pipeline; the channel's
+// logit sums plane by plane in the order sample_colour uses.  That takes
+// four times the rounds, whose vector instructions the one-lane march
+// (already bound by vector-ALU issue with many views) cannot spare, so
+// QUADS is set for rays of four or eight lanes.  Otherwise, or in a wave at
+// the image edge, one entry per lane.
+template <typename UT, int DC, bool LIN, int BS, bool QUADS>  // Eq. 4 only (LIN false)
 __device__ __forceinline__ void drain_colour(const RenderParams& P, const ColourQueue& cq, uint32_t& head,
                                              uint32_t n)
 {
     const uint64_t ex = __builtin_amdgcn_read_exec();
-    const uint32_t workers = static_cast<uint32_t>(__builtin_popcountll(ex));
-    const uint32_t rank = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(ex >> 32),
-                                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(ex), 0u));
-    for (uint32_t done = 0; done < n; done += workers) {
-        const uint32_t k = done + rank;
-        if (k < n) {
-            const uint4 e = cq.entries[(head + k) & (kQueue - 1)];
-            const uint32_t slot = e.x >> 26;
-            const uint32_t t0 = e.x & ((1u << 26) - 1u);
-            float col[3];
-            sample_colour<UT, DC, BS>(P, t0, e.y, e.z, cq.beta + slot, col);
-            const double w = static_cast<double>(__uint_as_float(e.w));
-            double* a = cq.acc + 3 * slot;
-            atomicAdd(a + 0, w * static_cast<double>(col[0]));
-            atomicAdd(a + 1, w * static_cast<double>(col[1]));
-            atomicAdd(a + 2, w * static_cast<double>(col[2]));
+    if (QUADS && ex == ~0ull) {
+        constexpr uint32_t NB = 3u * DC * static_cast<uint32_t>(sizeof(UT));   // bytes of a record
+        constexpr uint32_t CB = DC * static_cast<uint32_t>(sizeof(UT));        // bytes of a channel
+        constexpr int NQ = CB / 16;
+        static_assert(CB % 16 == 0, "channels of whole 16-byte pieces");
+        const uint32_t lane = __lane_id();
+        const uint32_t c = lane & 3u;
+        for (uint32_t done = 0; done < n; done += 16) {
+            const uint32_t k = done + (lane >> 2);
+            if (k < n && c < 3u) {
+                const uint4 e = cq.entries[(head + k) & (kQueue - 1)];
+                const uint32_t slot = e.x >> 26;
+                const uint32_t texel[3] = {e.x & ((1u << 26) - 1u), e.y, e.z};
+                const float* beta = cq.beta + slot;
+                float x = 0.0f;
+#pragma unroll
+                for (int j = 0; j < 3; ++j) {
+                    uint4 q[NQ];
+#pragma unroll
+                    for (int r = 0; r < NQ; ++r)
+                        q[r] = load_at<uint4>(P.uvw[j], texel[j] * NB + c * CB + 16u * r);
+                    UT rec[DC];
+                    __builtin_memcpy(rec, q, CB);
+#pragma unroll
+                    for (int r = 0; r < DC; ++r)
+                        x = fmaf(beta[r * BS], widen(rec[r]), x);
+                }
+                const double w = static_cast<double>(__uint_as_float(e.w));
+                atomicAdd(cq.acc + 3 * slot + c, w * static_cast<double>(sigmoid(x)));
+            }
+        }
+    } else {
+        const uint32_t workers = static_cast<uint32_t>(__builtin_popcountll(ex));
+        const uint32_t rank = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(ex >> 32),
+                                                        __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(ex), 0u));
+        for (uint32_t done = 0; done < n; done += workers) {
+            const uint32_t k = done + rank;
+            if (k < n) {
+                const uint4 e = cq.entries[(head + k) & (kQueue - 1)];
+                const uint32_t slot = e.x >> 26;
+                const uint32_t t0 = e.x & ((1u << 26) - 1u);
+                float col[3];
+                sample_colour<UT, DC, BS>(P, t0, e.y, e.z, cq.beta + slot, col);
+                const double w = static_cast<double>(__uint_as_float(e.w));
+                double* a = cq.acc + 3 * slot;
+                atomicAdd(a + 0, w * static_cast<double>(col[0]));
+                atomicAdd(a + 1, w * static_cast<double>(col[1]));
+                atomicAdd(a + 2, w * static_cast<double>(col[2]));
+            }
         }
     }
     head = (head + n) & (kQueue - 1);
@@ -1170,13 +1213,13 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
             // whole wave: count the pushes; evaluate 64 once they are waiting
             q_count += static_cast<uint32_t>(__builtin_popcountll(__builtin_amdgcn_ballot_w64(pushed)));
             if (q_count >= 64) {
-                drain_colour<UT, DC, LIN, BS>(P, cq, q_head, 64);
+                drain_colour<UT, DC, LIN, BS, (L > 1)>(P, cq, q_head, 64);
                 q_count -= 64;
             }
         }
     }
     if constexpr (kDefer)
-        drain_colour<UT, DC, LIN, BS>(P, cq, q_head, q_count);
+        drain_colour<UT, DC, LIN, BS, (L > 1)>(P, cq, q_head, q_count);
 
     // combine the lanes of the ray
     if constexpr (!kDefer) {
