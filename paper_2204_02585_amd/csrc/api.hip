@@ -334,8 +334,11 @@ CacheLayout cache_layout(const sqn_cache_desc* desc, bool linear)
     const int32_t D = desc->D;
     const size_t texels = static_cast<size_t>(desc->n_p) * desc->n_p;
     // packed records: 4 bytes for binary16 sigma, 8 for binary32 sigma or
-    // the linear decoder's binary32 partial sums
-    L.packed_bytes = texels * (!linear && desc->sigma_dtype == SQN_F16 ? 4 : 8);
+    // the linear decoder's binary32 partial sums; the product rule's planes
+    // interleave four rows (rows padded to a multiple of four), the linear
+    // decoder's stay row-major
+    const size_t rows = linear ? desc->n_p : (static_cast<size_t>(desc->n_p) + 3) / 4 * 4;
+    L.packed_bytes = rows * desc->n_p * (!linear && desc->sigma_dtype == SQN_F16 ? 4 : 8);
     L.uvw_bytes = texels * 3 * D * dtype_size(desc->uvw_dtype);
     L.beta_bytes = static_cast<size_t>(desc->n_theta) * desc->n_phi * D * dtype_size(desc->beta_dtype);
     L.lin_bytes = linear ? (9 * static_cast<size_t>(D) + 3) * D * sizeof(float) : 0;

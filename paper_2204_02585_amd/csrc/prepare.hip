@@ -86,21 +86,32 @@ __global__ void column_distance(const uint16_t* __restrict__ f, uint16_t* __rest
 }
 
 // Packed record: binary16 sigma -> one 32-bit word (sigma bits | dist << 16);
-// binary32 sigma -> two words (sigma bits, dist).
+// binary32 sigma -> two words (sigma bits, dist).  Record (a, b) of a plane
+// lands at (a & ~3) n_p + 4 b + (a & 3): four rows interleaved, so that a
+// 64-byte segment holds a 4 x 4 block of texels (4 x 2 with two-word
+// records), which a quad's four samples along a ray share far more often
+// than a run of one row (sigma_texel in render.hip); rows are padded to a
+// multiple of four.
+__device__ __forceinline__ uint32_t interleaved(uint32_t i, uint32_t n_p)
+{
+    const uint32_t a = i / n_p, b = i - a * n_p;
+    return (a & ~3u) * n_p + 4u * b + (a & 3u);
+}
+
 __global__ void pack_f16(const uint16_t* __restrict__ sigma, const uint16_t* __restrict__ dist,
-                         uint32_t* __restrict__ out, uint32_t n)
+                         uint32_t* __restrict__ out, uint32_t n, uint32_t n_p)
 {
     const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n)
-        out[i] = static_cast<uint32_t>(sigma[i]) | (static_cast<uint32_t>(dist[i]) << 16);
+        out[interleaved(i, n_p)] = static_cast<uint32_t>(sigma[i]) | (static_cast<uint32_t>(dist[i]) << 16);
 }
 
 __global__ void pack_f32(const uint32_t* __restrict__ sigma, const uint16_t* __restrict__ dist,
-                         uint2* __restrict__ out, uint32_t n)
+                         uint2* __restrict__ out, uint32_t n, uint32_t n_p)
 {
     const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n)
-        out[i] = make_uint2(sigma[i], static_cast<uint32_t>(dist[i]));
+        out[interleaved(i, n_p)] = make_uint2(sigma[i], static_cast<uint32_t>(dist[i]));
 }
 
 // Distance and packing of one plane whose live mask is in work.live.
@@ -345,10 +356,10 @@ hipError_t prepare_sigma_plane(const void* sigma, int sigma_dtype, int32_t n_p, 
         return e;
     if (sigma_dtype == SQN_F16)
         pack_f16<<<grid, 256, 0, stream>>>(static_cast<const uint16_t*>(sigma), work.dist,
-                                           static_cast<uint32_t*>(packed), n);
+                                           static_cast<uint32_t*>(packed), n, static_cast<uint32_t>(n_p));
     else
         pack_f32<<<grid, 256, 0, stream>>>(static_cast<const uint32_t*>(sigma), work.dist,
-                                           static_cast<uint2*>(packed), n);
+                                           static_cast<uint2*>(packed), n, static_cast<uint32_t>(n_p));
     return hipGetLastError();
 }
 

@@ -12,7 +12,8 @@ namespace sqn {
 // Everything one render launch reads, passed by value as the kernel argument.
 struct RenderParams {
     // caches (library-owned device memory)
-    const void* sigma[3];     // [n_p][n_p] packed (sigma, distance) records, planes xy, yz, zx
+    const void* sigma[3];     // packed (sigma, distance) records of planes xy, yz, zx: four rows
+                              // interleaved (prepare.hip) for Eq. 4, [n_p][n_p] for Eq. 5
     const void* uvw[3];       // [n_p][n_p][3D] records
     const void* beta;         // [n_theta][n_phi][D]
     // camera batch and outputs (caller-owned device memory)
