@@ -334,10 +334,9 @@ CacheLayout cache_layout(const sqn_cache_desc* desc, bool linear)
     const int32_t D = desc->D;
     const size_t texels = static_cast<size_t>(desc->n_p) * desc->n_p;
     // packed records: 4 bytes for binary16 sigma, 8 for binary32 sigma or
-    // the linear decoder's binary32 partial sums; the product rule's planes
-    // interleave four rows (rows padded to a multiple of four), the linear
-    // decoder's stay row-major
-    const size_t rows = linear ? desc->n_p : (static_cast<size_t>(desc->n_p) + 3) / 4 * 4;
+    // the linear decoder's binary32 partial sums, four rows interleaved
+    // (rows padded to a multiple of four)
+    const size_t rows = (static_cast<size_t>(desc->n_p) + 3) / 4 * 4;
     L.packed_bytes = rows * desc->n_p * (!linear && desc->sigma_dtype == SQN_F16 ? 4 : 8);
     L.uvw_bytes = texels * 3 * D * dtype_size(desc->uvw_dtype);
     L.beta_bytes = static_cast<size_t>(desc->n_theta) * desc->n_phi * D * dtype_size(desc->beta_dtype);
@@ -426,6 +425,8 @@ sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec
     work_total += align(cells * sizeof(uint16_t));
     const size_t w_cf2 = work_total;
     work_total += align(cells * sizeof(uint16_t));
+    const size_t w_rows = work_total;
+    work_total += align(linear ? texels * sizeof(uint2) : 0);
 
     // host-side parameters of the linear decoder: W_sigma, and the radiance
     // weights transposed so that row c*3D + e holds W_c[0..D)[e], followed
@@ -483,6 +484,7 @@ sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec
     pw.cell_live = reinterpret_cast<uint8_t*>(work + w_clive);
     pw.cell_f = reinterpret_cast<uint16_t*>(work + w_cf);
     pw.cell_f2 = reinterpret_cast<uint16_t*>(work + w_cf2);
+    pw.rows = reinterpret_cast<uint2*>(work + w_rows);
 
     void* packed[3];
     for (int j = 0; j < 3; ++j) {
@@ -502,6 +504,8 @@ sqn_status create_impl(const sqn_cache_desc* desc, const sqn_linear_decoder* dec
         if (e == hipSuccess)
             e = sqn::prepare_linear_cells(packed, desc->n_p, dec->b_sigma, cell_shift, cell_m,
                                           reinterpret_cast<uint8_t*>(base + off_cells), pw, st);
+        if (e == hipSuccess)
+            e = sqn::interleave_linear_planes(packed, desc->n_p, pw, st);
     } else {
         for (int j = 0; j < 3 && e == hipSuccess; ++j)
             e = sqn::prepare_sigma_plane(sigma_planes[j], desc->sigma_dtype, desc->n_p, packed[j], pw, st);

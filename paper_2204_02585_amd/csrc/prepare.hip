@@ -91,7 +91,9 @@ __global__ void column_distance(const uint16_t* __restrict__ f, uint16_t* __rest
 // 64-byte segment holds a 4 x 4 block of texels (4 x 2 with two-word
 // records), which a quad's four samples along a ray share far more often
 // than a run of one row (sigma_texel in render.hip); rows are padded to a
-// multiple of four.
+// multiple of four.  The linear decoder's planes are built row-major (their
+// passes read rows and columns) and interleaved at the end
+// (interleave_linear_planes).
 __device__ __forceinline__ uint32_t interleaved(uint32_t i, uint32_t n_p)
 {
     const uint32_t a = i / n_p, b = i - a * n_p;
@@ -104,6 +106,14 @@ __global__ void pack_f16(const uint16_t* __restrict__ sigma, const uint16_t* __r
     const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n)
         out[interleaved(i, n_p)] = static_cast<uint32_t>(sigma[i]) | (static_cast<uint32_t>(dist[i]) << 16);
+}
+
+__global__ void scatter_interleaved(const uint2* __restrict__ rows, uint2* __restrict__ out, uint32_t n,
+                                    uint32_t n_p)
+{
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n)
+        out[interleaved(i, n_p)] = rows[i];
 }
 
 __global__ void pack_f32(const uint32_t* __restrict__ sigma, const uint16_t* __restrict__ dist,
@@ -397,6 +407,24 @@ hipError_t prepare_linear_planes(const void* const sigma[3], int sigma_dtype, in
         if ((e = distance_transform(n_p, work, stream)) != hipSuccess)
             return e;
         set_distance<<<grid, 256, 0, stream>>>(work.dist, rec, n);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t interleave_linear_planes(void* const packed[3], int32_t n_p, const PrepareWork& work,
+                                    hipStream_t stream)
+{
+    const uint32_t n = static_cast<uint32_t>(n_p) * static_cast<uint32_t>(n_p);
+    const dim3 grid((n + 255) / 256);
+    for (int j = 0; j < 3; ++j) {
+        hipError_t e = hipMemcpyAsync(work.rows, packed[j], static_cast<size_t>(n) * sizeof(uint2),
+                                      hipMemcpyDeviceToDevice, stream);
+        if (e != hipSuccess)
+            return e;
+        scatter_interleaved<<<grid, 256, 0, stream>>>(work.rows, static_cast<uint2*>(packed[j]), n,
+                                                      static_cast<uint32_t>(n_p));
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
     }

@@ -714,20 +714,15 @@ __device__ __forceinline__ void drain_colour(const RenderParams& P, const Colour
 // distance (texels) to the nearest texel with sigma^j != 0 (0 = this one),
 // see prepare.hip.  binary16 sigma: one word (sigma | dist << 16); binary32
 // sigma: two words.
-// Position of record (a, b) in a packed plane.  The product rule's planes
-// interleave four rows, (a & ~3) n_p + 4 b + (a & 3), so a 64-byte segment
-// holds a 4 x 4 block of texels (4 x 2 with two-word records): the four
-// samples of a ray that a quad gathers together, a texel or two apart,
-// touch 2.3 segments per plane on an 800 x 800 view against 3.6 in
-// row-major order, and a gather costs the memory pipeline by segments.
-// The linear decoder's planes stay row-major.
-template <bool LIN>
+// Position of record (a, b) in a packed plane: four rows interleaved,
+// (a & ~3) n_p + 4 b + (a & 3), so a 64-byte segment holds a 4 x 4 block of
+// texels (4 x 2 with two-word records): the four samples of a ray that a
+// quad gathers together, a texel or two apart, touch 2.3 segments per plane
+// on an 800 x 800 view against 3.6 in row-major order (2.9 against 3.6 with
+// two-word records), and a gather costs the memory pipeline by segments.
 __device__ __forceinline__ uint32_t sigma_texel(uint32_t a, uint32_t b, uint32_t n_p)
 {
-    if constexpr (LIN)
-        return __umul24(a, n_p) + b;
-    else
-        return __umul24(a & ~3u, n_p) + ((b << 2) | (a & 3u));
+    return __umul24(a & ~3u, n_p) + ((b << 2) | (a & 3u));
 }
 
 template <typename ST>
@@ -1074,9 +1069,9 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
             if (!dead) {
                 float sxy, syz, szx;
                 uint32_t dxy, dyz, dzx;
-                SigmaRecord<ST>::load(P.sigma[0], sigma_texel<LIN>(ix, iy, n_p), sxy, dxy);
-                SigmaRecord<ST>::load(P.sigma[1], sigma_texel<LIN>(iy, iz, n_p), syz, dyz);
-                SigmaRecord<ST>::load(P.sigma[2], sigma_texel<LIN>(iz, ix, n_p), szx, dzx);
+                SigmaRecord<ST>::load(P.sigma[0], sigma_texel(ix, iy, n_p), sxy, dxy);
+                SigmaRecord<ST>::load(P.sigma[1], sigma_texel(iy, iz, n_p), syz, dyz);
+                SigmaRecord<ST>::load(P.sigma[2], sigma_texel(iz, ix, n_p), szx, dzx);
                 if constexpr (LIN) {
                     // Eq. 5 on the folded per-plane partial sums
                     float pre = sxy + syz;

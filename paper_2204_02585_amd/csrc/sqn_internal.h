@@ -12,8 +12,8 @@ namespace sqn {
 // Everything one render launch reads, passed by value as the kernel argument.
 struct RenderParams {
     // caches (library-owned device memory)
-    const void* sigma[3];     // packed (sigma, distance) records of planes xy, yz, zx: four rows
-                              // interleaved (prepare.hip) for Eq. 4, [n_p][n_p] for Eq. 5
+    const void* sigma[3];     // packed (sigma, distance) records of planes xy, yz, zx, four rows
+                              // interleaved (prepare.hip)
     const void* uvw[3];       // [n_p][n_p][3D] records
     const void* beta;         // [n_theta][n_phi][D]
     // camera batch and outputs (caller-owned device memory)
@@ -80,6 +80,7 @@ struct PrepareWork {
     uint8_t* cell_live;   // [m^3]
     uint16_t* cell_f;     // [m^3] partial distances
     uint16_t* cell_f2;    // [m^3]
+    uint2* rows;          // [n_p^2] row-major copy of a linear decoder's plane
 };
 
 // Pack sigma plane j (n_p x n_p of sigma_dtype, device memory) into
@@ -106,6 +107,11 @@ hipError_t prepare_linear_planes(const void* const sigma[3], int sigma_dtype, in
 // floats, work.cell_live m^3 bytes, work.cell_f / cell_g2 m^3 uint16 each.
 hipError_t prepare_linear_cells(const void* const packed[3], int32_t n_p, float b_sigma, int32_t shift,
                                 int32_t m, uint8_t* cell_dist, const PrepareWork& work, hipStream_t stream);
+
+// Move the linear decoder's packed planes (row-major after the passes
+// above) into the interleaved order the renderer reads, through work.rows.
+hipError_t interleave_linear_planes(void* const packed[3], int32_t n_p, const PrepareWork& work,
+                                    hipStream_t stream);
 
 // Cell side 2^shift for an n_p grid: the smallest power of two >= 2 that
 // leaves at most 128 cells per axis.
