@@ -714,15 +714,24 @@ __device__ __forceinline__ void drain_colour(const RenderParams& P, const Colour
 // distance (texels) to the nearest texel with sigma^j != 0 (0 = this one),
 // see prepare.hip.  binary16 sigma: one word (sigma | dist << 16); binary32
 // sigma: two words.
-// Position of record (a, b) in a packed plane: four rows interleaved,
-// (a & ~3) n_p + 4 b + (a & 3), so a 64-byte segment holds a 4 x 4 block of
-// texels (4 x 2 with two-word records): the four samples of a ray that a
-// quad gathers together, a texel or two apart, touch 2.3 segments per plane
-// on an 800 x 800 view against 3.6 in row-major order (2.9 against 3.6 with
-// two-word records), and a gather costs the memory pipeline by segments.
-__device__ __forceinline__ uint32_t sigma_texel(uint32_t a, uint32_t b, uint32_t n_p)
+// Byte offset of record (a, b) in a packed plane of B-byte records, four
+// rows interleaved: B ((a & ~3) n_p + 4 b + (a & 3)), so a 64-byte segment
+// holds a 4 x 4 block of texels (4 x 2 with two-word records): the four
+// samples of a ray that a quad gathers together, a texel or two apart,
+// touch 2.3 segments per plane on an 800 x 800 view against 3.6 in
+// row-major order (2.9 against 3.6 with two-word records), and a gather
+// costs the memory pipeline by segments.  Written as row_part(a) + 4 B b
+// with row_part(a) = B ((n_p - 1)(a & ~3) + a), each coordinate's part
+// shared by its plane; bnm1 = B (n_p - 1).
+template <uint32_t B>
+__device__ __forceinline__ uint32_t row_part(uint32_t a, uint32_t bnm1)
 {
-    return __umul24(a & ~3u, n_p) + ((b << 2) | (a & 3u));
+    return __umul24(a & ~3u, bnm1) + a * B;
+}
+template <uint32_t B>
+__device__ __forceinline__ uint32_t record_offset(uint32_t row_a, uint32_t b)
+{
+    return row_a + b * (4u * B);
 }
 
 template <typename ST>
@@ -731,9 +740,9 @@ struct SigmaRecord;
 template <>
 struct SigmaRecord<_Float16> {
     static constexpr uint32_t bytes = 4;
-    static __device__ __forceinline__ void load(const void* plane, uint32_t texel, float& sigma, uint32_t& dist)
+    static __device__ __forceinline__ void load(const void* plane, uint32_t off, float& sigma, uint32_t& dist)
     {
-        const uint32_t w = load_at<uint32_t>(plane, texel * bytes);
+        const uint32_t w = load_at<uint32_t>(plane, off);
         sigma = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w & 0xffffu)));
         dist = w >> 16;
     }
@@ -742,9 +751,9 @@ struct SigmaRecord<_Float16> {
 template <>
 struct SigmaRecord<float> {
     static constexpr uint32_t bytes = 8;
-    static __device__ __forceinline__ void load(const void* plane, uint32_t texel, float& sigma, uint32_t& dist)
+    static __device__ __forceinline__ void load(const void* plane, uint32_t off, float& sigma, uint32_t& dist)
     {
-        const uint2 w = load_at<uint2>(plane, texel * bytes);
+        const uint2 w = load_at<uint2>(plane, off);
         sigma = __uint_as_float(w.x);
         dist = w.y;
     }
@@ -773,16 +782,17 @@ __device__ __forceinline__ float leap_index(const RenderParams& P, float t_exit)
 // plane's two axes the grid coordinate g = (p - bmin) scale moves affinely in
 // t (g = g0 + t ds), and the node index stays inside the square while g is
 // below c + D - 1/2 (or above c - D + 1/2 moving down).  The bound is pulled
-// in by `margin` texels (the binary32 position and rounding error of g), so
-// every sample up to the exit parameter is inside the square.
+// in by a margin of texels (the binary32 position and rounding error of g),
+// so every sample up to the exit parameter is inside the square; `half` is
+// 1/2 + that margin, formed once per ray.
 // inv_ds[r] = 1 / ds[r], +inf for ds = 0, so that an axis the ray does not
 // move along never ends the run (a non-positive distance to the bound there
 // gives -inf or NaN, i.e. no leap or the other axis: never a longer one);
 // its sign tells the direction.
 __device__ __forceinline__ int32_t leap_target(const RenderParams& P, int j, uint32_t D, const uint32_t c[3],
-                                               const float g0[3], const float inv_ds[3], float margin, int32_t i)
+                                               const float g0[3], const float inv_ds[3], float half, int32_t i)
 {
-    const float h = static_cast<float>(D) - 0.5f - margin;
+    const float h = static_cast<float>(D) - half;
     float t[3];
 #pragma unroll
     for (int r = 0; r < 3; ++r) {
@@ -794,8 +804,10 @@ __device__ __forceinline__ int32_t leap_target(const RenderParams& P, int j, uin
     const float t01 = fminf(t[0], t[1]), t12 = fminf(t[1], t[2]), t20 = fminf(t[2], t[0]);
     const float t_exit = j == 0 ? t01 : (j == 1 ? t12 : t20);
     const float f = leap_index(P, t_exit);
+    // clamp to [i + 1, N]; a NaN f gives i + 1 (the median of three takes
+    // the smallest when an operand is NaN)
     const float lo = static_cast<float>(i + 1), hi = static_cast<float>(P.n_samples);
-    return static_cast<int32_t>(fminf(fmaxf(f, lo), hi));
+    return static_cast<int32_t>(__builtin_amdgcn_fmed3f(f, lo, hi));
 }
 
 // First sample index a leap may land on after sample i, whose node indices
@@ -859,7 +871,8 @@ struct RayGeom {
     float g0[3], inv_ds[3];   // grid coordinate g = g0 + t ds per axis, 1/ds
     float margin;             // texels a leap keeps from its square's edge
     int32_t i0, i1;           // samples that may lie in the box
-    int32_t j0, j1;           // samples certainly in the box
+    int32_t j0;               // samples certainly in the box: i - j0 <= jspan as unsigned
+    uint32_t jspan;           // (j0 = INT_MIN, jspan = 0 when there are none)
 };
 
 // World ray through the pixel centre of (u, v) (camera looks down -z).
@@ -898,14 +911,21 @@ __device__ __forceinline__ void march_geometry(const RenderParams& P, const floa
         no_samples = !ndc_ray(P, g.o, g.d);
     const float d00 = g.d[0] * g.d[0], d11 = g.d[1] * g.d[1], d22 = g.d[2] * g.d[2];
     g.dn = sqrtf((d00 + d11) + d22);
-    clip_to_box(P, g.o, g.d, g.i0, g.i1, g.j0, g.j1);
+    int32_t j1;
+    clip_to_box(P, g.o, g.d, g.i0, g.i1, g.j0, j1);
     if constexpr (NDC) {
         if (no_samples) {
             g.i0 = 1;
             g.i1 = 0;
             g.j0 = 1;
-            g.j1 = 0;
+            j1 = 0;
         }
+    }
+    if (g.j0 <= j1) {
+        g.jspan = static_cast<uint32_t>(j1 - g.j0);
+    } else {
+        g.j0 = INT32_MIN;
+        g.jspan = 0;
     }
     g.margin = 0.0f;
     if constexpr (SKIP) {
@@ -983,10 +1003,12 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
     const float* const o = geo.o;
     const float* const d = geo.d;
     const float dn = geo.dn;
-    const int32_t i0 = geo.i0, i1 = geo.i1, j0 = geo.j0, j1 = geo.j1;
+    const int32_t i0 = geo.i0, i1 = geo.i1, j0 = geo.j0;
+    const uint32_t jspan = geo.jspan;
     const float* const g0 = geo.g0;
     const float* const inv_ds = geo.inv_ds;
     const float leap_margin = geo.margin;
+    const float leap_half = 0.5f + leap_margin;
     const int32_t n_p = P.n_p;
     const float hi_node = static_cast<float>(n_p - 1);
     // Eq. 4 at D = 8 defers colour to the wave's queue (measured: 4-8%
@@ -1037,7 +1059,8 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
         // when every lane's sample is certainly in the box the six exact
         // tests would all pass and the node indices need no clamp (a
         // wave-uniform branch)
-        const bool deep = (i >= j0) & (i <= j1);
+        // 0 <= i - j0 <= jspan, one unsigned compare (i >= 0 > INT_MIN)
+        const bool deep = static_cast<uint32_t>(i) - static_cast<uint32_t>(j0) <= jspan;
         if (__builtin_amdgcn_ballot_w64(deep) == __builtin_amdgcn_read_exec()) {
             inside = true;
             ix = nearest_node_inside(p[0], P.bmin[0], P.scale[0]);
@@ -1069,9 +1092,11 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
             if (!dead) {
                 float sxy, syz, szx;
                 uint32_t dxy, dyz, dzx;
-                SigmaRecord<ST>::load(P.sigma[0], sigma_texel(ix, iy, n_p), sxy, dxy);
-                SigmaRecord<ST>::load(P.sigma[1], sigma_texel(iy, iz, n_p), syz, dyz);
-                SigmaRecord<ST>::load(P.sigma[2], sigma_texel(iz, ix, n_p), szx, dzx);
+                constexpr uint32_t RB = SigmaRecord<ST>::bytes;
+                const uint32_t bnm1 = RB * static_cast<uint32_t>(n_p - 1);
+                SigmaRecord<ST>::load(P.sigma[0], record_offset<RB>(row_part<RB>(ix, bnm1), iy), sxy, dxy);
+                SigmaRecord<ST>::load(P.sigma[1], record_offset<RB>(row_part<RB>(iy, bnm1), iz), syz, dyz);
+                SigmaRecord<ST>::load(P.sigma[2], record_offset<RB>(row_part<RB>(iz, bnm1), ix), szx, dzx);
                 if constexpr (LIN) {
                     // Eq. 5 on the folded per-plane partial sums
                     float pre = sxy + syz;
@@ -1089,7 +1114,7 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
                     if (dmax != 0) {
                         const int j = (dxy == dmax) ? 0 : ((dyz == dmax) ? 1 : 2);
                         const uint32_t c[3] = {ix, iy, iz};
-                        leap = leap_target(P, j, dmax, c, g0, inv_ds, leap_margin, i);
+                        leap = leap_target(P, j, dmax, c, g0, inv_ds, leap_half, i);
                     }
                 }
             }
