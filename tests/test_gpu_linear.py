@@ -59,6 +59,16 @@ def test_alt_component_counts_and_dtypes(D, dtype, mode):
 
 
 @pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("n_p", [6, 7, 13, 50])
+def test_alt_plane_sizes_not_multiple_of_four(n_p, mode):
+    """The Eq. 5 planes are moved into the four-row interleaved order at
+    creation, the last group of rows padded."""
+    sc = _small(n_p=n_p, width=32, height=24, focal=40.0)
+    ref = _full_frame(sc, mode, f"alt n_p={n_p} {mode}")
+    assert ref["n_occ"].sum() > 0
+
+
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("d_sigma", [1, 5, 64])
 def test_alt_density_channel_counts(d_sigma, mode):
     sc = _small(sigma_channels=d_sigma, width=40, height=24, focal=50.0)

@@ -76,6 +76,20 @@ def test_component_counts_and_dtypes(D, dtype, mode):
     pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), f"D={D} {dtype}")
 
 
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("sigma_dtype", ["f16", "f32"])
+@pytest.mark.parametrize("n_p", [2, 5, 6, 7, 13, 50])
+def test_plane_sizes_not_multiple_of_four(n_p, sigma_dtype, mode):
+    """The packed sigma planes interleave four rows and pad the last group:
+    plane sizes that are not a multiple of four, with one-word (binary16)
+    and two-word (binary32) records.  At n_p = 2 no sample is occupied."""
+    sc = _small("tiny", width=32, height=32, n_p=n_p, dtype="f16", sigma_dtype=sigma_dtype)
+    gpu = pu.gpu_render(sc, mode=mode)
+    ref = oracle.render_scene(sc)
+    pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), f"n_p={n_p} sigma {sigma_dtype}")
+    assert (ref["n_occ"].sum() > 0) == (n_p > 2)
+
+
 def test_paper_precision_mix():
     """sigma^j in fp32, u^j v^j w^j and beta in fp16 (Sec. 3.3)."""
     sc = _small("tiny", width=48, height=48)
