@@ -60,13 +60,14 @@ TD_PEAK_GCYCLES = 256 * 2.4
 CLOCK_GHZ = 2.4
 
 
-def counter_record(config_name, kind="render"):
+def counter_record(config_name, kind="render", lanes=None):
     """The committed rocprofv3 counter record of a workload's kernel
     (profiles/<kind>_traffic_<workload>.json): HBM bytes per launch from the
     FETCH_SIZE / WRITE_SIZE passes scaled by kernels of known traffic, and
     for render kernels the TD busy cycles, L1 accesses and VALU
-    instructions per launch.  None when no such file exists or the kernel
-    source has changed since the counters were taken."""
+    instructions per launch.  None when no such file exists, the kernel
+    source has changed since the counters were taken, or (lanes given) the
+    record is of a kernel with another number of lanes per ray."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"{kind}_traffic_{config_name}.json")
     src = os.path.join(ROOT, "paper_2204_02585_amd", "csrc", f"{kind}.hip")
@@ -76,6 +77,8 @@ def counter_record(config_name, kind="render"):
     except (OSError, ValueError):
         return None
     if rec.get(f"{kind}_hip_sha256_16") != sha:
+        return None
+    if lanes and f"L={lanes}," not in rec.get("kernel", ""):
         return None
     return rec
 
@@ -381,6 +384,8 @@ def main():
                     help="lanes of a wavefront per ray (1, 4 or 8); 0 = the library's choice")
     ap.add_argument("--dense", action="store_true",
                     help="march every sample (no leaps over empty space)")
+    ap.add_argument("--no-tune", action="store_true",
+                    help="with --lanes 0, keep the library's per-call choice instead of timing the shapes")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the ceiling probes (memory levels; matrix cores for gen_*)")
@@ -422,6 +427,13 @@ def main():
     depth = torch.empty((B, cfg.height, cfg.width), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
     N = cfg.n_samples
+    lanes = args.lanes
+    if lanes == 0 and not args.no_tune:
+        # the library times its launch shapes on this batch and keeps the
+        # fastest (outside the timed region, like any warm-up)
+        print("[bench] tuning lanes per ray", file=sys.stderr, flush=True)
+        lanes = caches.tune_lanes_per_ray(poses, scene.intrinsics, scene.near, scene.far, N, rgb, depth,
+                                          stream=stream)
 
     # untimed diagnostics pass: live / occupied sample counts for the byte model
     _, _, st = caches.render_stats(poses, scene.intrinsics, scene.near, scene.far, N)
@@ -502,7 +514,8 @@ def main():
                    "direction_cache": [cfg.n_theta, cfg.n_phi], "t_eps": cfg.t_eps,
                    "decoder": ("Eq. 5 linear, D_sigma=%d" % cfg.sigma_channels
                                if cfg.sigma_channels > 0 else "Eq. 4 product/sum"),
-                   "lanes_per_ray": args.lanes or "auto",
+                   "lanes_per_ray": (f"tuned: {lanes}" if args.lanes == 0 and not args.no_tune
+                                     else (args.lanes or "auto")),
                    "empty_space_leaps": not args.dense},
         "frames_per_s": round(fps, 2),
         "samples": {"nominal_per_step": nominal, "live_inbox_per_step": live_inbox,
@@ -510,8 +523,8 @@ def main():
                     "empty_fraction_of_live_inbox": round(1.0 - occupied / live_inbox, 4) if live_inbox else None,
                     "live_inbox_msamples_per_s": round(live_inbox / (ms * 1e-3) / 1e6, 1),
                     "occupied_msamples_per_s": round(occupied / (ms * 1e-3) / 1e6, 1)},
-        "roofline": render_roofline(counter_record(cfg.name) if args.lanes == 0 and not args.dense else None,
-                                    ms, bytes_alg),
+        "roofline": render_roofline(counter_record(cfg.name, lanes=lanes) if args.lanes == 0 and not args.dense
+                                    else None, ms, bytes_alg),
         "cpu_baseline": base,
         "ceilings": ceilings,
         "wall_s_timed": round(wall, 4),

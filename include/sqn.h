@@ -233,6 +233,28 @@ sqn_status sqn_render_stats(const sqn_caches* caches,
  * made by sqn_create_linear_caches (always four lanes). */
 sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes);
 
+/* Measure the launch shapes on one batch and keep the fastest: renders the
+ * batch (arguments as sqn_render) with 4, 1 and 8 lanes per ray (four only
+ * for a handle made by sqn_create_linear_caches), each once untimed and five
+ * times between two HIP events on `stream`, then sets the handle's lanes
+ * per ray as sqn_set_lanes_per_ray would and, if lanes_out is not NULL,
+ * writes the choice there (for an empty batch the setting stays).  No
+ * candidate changes a sample, index or termination decision, only the
+ * time; which is fastest depends on the image size, the number of views and
+ * the scene (the chains of samples), which the default per-call choice sees
+ * only through the number of rays.  A single view rendered with one lane
+ * per ray deals its tiles from the centre of the image outwards (the long
+ * rays over a centred object first).  rgb_out and depth_out receive a
+ * render of the batch.  Blocks until the timed renders finish; creates two
+ * HIP events and allocates no device memory.  Not thread-safe against
+ * concurrent renders with the handle.  Errors: those of sqn_render (the
+ * handle's setting is then left as it was); SQN_ERR_DEVICE if the events
+ * fail. */
+sqn_status sqn_tune_lanes_per_ray(sqn_caches* caches, const float* poses, int32_t n_poses,
+                                  const sqn_intrinsics* intrinsics, float near_plane, float far_plane,
+                                  int32_t n_samples, float* rgb_out, float* depth_out, void* stream,
+                                  int32_t* lanes_out);
+
 /* Leaps over empty space (1, the default) or a dense march (0).  sigma is
  * the product of the three planar sigma^j (Sec. 3.2 Eq. 4), so it vanishes
  * wherever one plane does; sqn_create_caches stores, next to each sigma^j,

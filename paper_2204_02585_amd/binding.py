@@ -19,7 +19,7 @@ SQN_OK, SQN_ERR_INVALID_ARG, SQN_ERR_OUT_OF_MEMORY, SQN_ERR_DEVICE, SQN_ERR_UNSU
 SQN_F32, SQN_F16 = 0, 1
 
 EXPORTS = ("sqn_create_caches", "sqn_create_linear_caches", "sqn_recreate_caches", "sqn_render", "sqn_render_stats",
-           "sqn_set_lanes_per_ray", "sqn_set_empty_space_skipping", "sqn_set_ndc", "sqn_cache_device_bytes",
+           "sqn_set_lanes_per_ray", "sqn_tune_lanes_per_ray", "sqn_set_empty_space_skipping", "sqn_set_ndc", "sqn_cache_device_bytes",
            "sqn_destroy", "sqn_status_string", "sqn_last_error", "sqn_create_networks",
            "sqn_generate_caches", "sqn_networks_device_bytes", "sqn_destroy_networks")
 
@@ -93,6 +93,9 @@ def _load() -> ctypes.CDLL:
                                      vp, vp, vp, vp]
     lib.sqn_set_lanes_per_ray.restype = ctypes.c_int
     lib.sqn_set_lanes_per_ray.argtypes = [vp, i32]
+    lib.sqn_tune_lanes_per_ray.restype = ctypes.c_int
+    lib.sqn_tune_lanes_per_ray.argtypes = [vp, vp, i32, ctypes.POINTER(Intrinsics), f32, f32, i32, vp, vp, vp,
+                                           ctypes.POINTER(i32)]
     lib.sqn_set_empty_space_skipping.restype = ctypes.c_int
     lib.sqn_set_empty_space_skipping.argtypes = [vp, i32]
     lib.sqn_set_ndc.restype = ctypes.c_int
@@ -269,6 +272,29 @@ class Caches:
     def set_lanes_per_ray(self, lanes: int) -> None:
         """1, 4 or 8 lanes of a wavefront per ray, or 0 to choose per call."""
         _check(lib.sqn_set_lanes_per_ray(self.handle, int(lanes)))
+
+    def tune_lanes_per_ray(self, poses: torch.Tensor, intrinsics: dict, near: float, far: float,
+                           n_samples: int, rgb_out: Optional[torch.Tensor] = None,
+                           depth_out: Optional[torch.Tensor] = None, stream=None) -> int:
+        """sqn_tune_lanes_per_ray: time the lanes-per-ray choices on this
+        batch, keep the fastest for later renders and return it.  Blocks;
+        rgb_out / depth_out (allocated if not given) receive a render."""
+        poses = _poses_arg(poses)
+        B = poses.shape[0]
+        H, W = int(intrinsics["height"]), int(intrinsics["width"])
+        if rgb_out is None:
+            rgb_out = torch.empty((B, H, W, 3), dtype=torch.float32, device=poses.device)
+        if depth_out is None:
+            depth_out = torch.empty((B, H, W), dtype=torch.float32, device=poses.device)
+        _output_arg(rgb_out, (B, H, W, 3), poses.device, "rgb_out")
+        _output_arg(depth_out, (B, H, W), poses.device, "depth_out")
+        _order_after_current(stream, poses, rgb_out, depth_out)
+        intr = _intrinsics(intrinsics)
+        chosen = ctypes.c_int32(0)
+        _check(lib.sqn_tune_lanes_per_ray(self.handle, _ptr(poses), B, ctypes.byref(intr), float(near),
+                                          float(far), int(n_samples), _ptr(rgb_out), _ptr(depth_out),
+                                          _stream(stream), ctypes.byref(chosen)))
+        return int(chosen.value)
 
     def set_empty_space_skipping(self, enable: bool) -> None:
         """Leaps over empty space (default) or a dense march."""

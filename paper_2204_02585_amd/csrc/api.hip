@@ -309,6 +309,9 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
     if (groups > std::numeric_limits<int32_t>::max())
         return fail(SQN_ERR_INVALID_ARG, "too many workgroups (%lld)", static_cast<long long>(groups));
     p.n_groups = static_cast<int32_t>(groups);
+    // centre-out tile order: measured faster for one view with one lane per
+    // ray (shorter tail), slower for batches of views and with 4 or 8 lanes
+    p.centre_out = (p.lanes == 1 && n_poses == 1) ? 1 : 0;
 
     // the linear decoder's records hold binary32 partial sums
     const int sigma_records = h->linear ? SQN_F32 : h->desc.sigma_dtype;
@@ -1004,6 +1007,72 @@ sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes)
     if (caches->linear && (lanes == 1 || lanes == 8))
         return fail(SQN_ERR_UNSUPPORTED, "the linear decoder renders with four lanes per ray");
     caches->lanes = lanes;
+    return SQN_OK;
+}
+
+sqn_status sqn_tune_lanes_per_ray(sqn_caches* caches, const float* poses, int32_t n_poses,
+                                  const sqn_intrinsics* intrinsics, float near_plane, float far_plane,
+                                  int32_t n_samples, float* rgb_out, float* depth_out, void* stream,
+                                  int32_t* lanes_out)
+{
+    if (!caches)
+        return fail(SQN_ERR_INVALID_ARG, "caches is NULL");
+    const int32_t before = caches->lanes;
+    // the batch itself is checked by the first render
+    static const int32_t kCandidates[3] = {4, 1, 8};
+    const int n_cand = caches->linear ? 1 : 3;
+    constexpr int kReps = 5;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    for (int k = 0; k < 2; ++k)
+        if (hipEventCreate(&ev[k]) != hipSuccess) {
+            (void)hipGetLastError();
+            if (ev[0])
+                (void)hipEventDestroy(ev[0]);
+            return fail(SQN_ERR_DEVICE, "hipEventCreate failed");
+        }
+    sqn_status s = SQN_OK;
+    int32_t best = kCandidates[0];
+    float best_ms = INFINITY;
+    for (int c = 0; c < n_cand && s == SQN_OK; ++c) {
+        caches->lanes = kCandidates[c];
+        // one untimed call (code and caches warm), then kReps timed ones
+        s = render_common(caches, poses, n_poses, intrinsics, near_plane, far_plane, n_samples, rgb_out,
+                          depth_out, nullptr, stream);
+        if (s != SQN_OK || n_poses == 0)
+            break;
+        hipError_t e = hipEventRecord(ev[0], st);
+        for (int r = 0; r < kReps && s == SQN_OK && e == hipSuccess; ++r)
+            s = render_common(caches, poses, n_poses, intrinsics, near_plane, far_plane, n_samples, rgb_out,
+                              depth_out, nullptr, stream);
+        if (s != SQN_OK)
+            break;
+        if (e == hipSuccess)
+            e = hipEventRecord(ev[1], st);
+        if (e == hipSuccess)
+            e = hipEventSynchronize(ev[1]);
+        float ms = 0.0f;
+        if (e == hipSuccess)
+            e = hipEventElapsedTime(&ms, ev[0], ev[1]);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            s = fail(SQN_ERR_DEVICE, "timing the launch shapes failed: %s", hipGetErrorString(e));
+            break;
+        }
+        if (ms < best_ms) {
+            best_ms = ms;
+            best = kCandidates[c];
+        }
+    }
+    (void)hipEventDestroy(ev[0]);
+    (void)hipEventDestroy(ev[1]);
+    if (s != SQN_OK) {
+        caches->lanes = before;
+        return s;
+    }
+    caches->lanes = n_poses == 0 ? before : best;
+    if (lanes_out)
+        *lanes_out = caches->lanes;
     return SQN_OK;
 }
 

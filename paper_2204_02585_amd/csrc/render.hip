@@ -1357,8 +1357,18 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) 
     const int32_t tiles_per_view = P.tiles_x * P.tiles_y;
     const int32_t view = tile / tiles_per_view;
     const int32_t tr = tile - view * tiles_per_view;
-    const int32_t ty = tr / P.tiles_x;
-    const int32_t tx = tr - ty * P.tiles_x;
+    int32_t ty = tr / P.tiles_x;
+    int32_t tx = tr - ty * P.tiles_x;
+    if (P.centre_out) {
+        // one view with one lane per ray: its time is set by the waves with
+        // the longest chains of samples, which sit over the middle of the
+        // image for a centred object, so those tiles go first and the light
+        // edge tiles fill the end of the launch; k -> n/2, n/2 - 1, n/2 + 1,
+        // ... is a bijection of [0, n)
+        auto centre = [](int32_t k, int32_t n) { return (k & 1) == 0 ? n / 2 + k / 2 : n / 2 - 1 - k / 2; };
+        ty = centre(ty, P.tiles_y);
+        tx = centre(tx, P.tiles_x);
+    }
     constexpr int32_t WW = kWaveW(L), WH = kWaveH(L);
     const int32_t slot = lane / L;
     const int32_t u = tx * kTileW(L) + (wave & 1) * WW + (slot % WW);

@@ -47,6 +47,7 @@ struct RenderParams {
     float leap_margin;        // texels a leap keeps from its square's edge
     int32_t tiles_x, tiles_y; // workgroup tiles per view
     int32_t n_groups;         // workgroups in the grid
+    int32_t centre_out;       // 1: tile rows and columns dealt from the image centre outwards
     // linear (Eq. 5) decoder; sigma[j] then holds per-plane partial sums
     int32_t linear;           // 1: Eq. 5, 0: Eq. 4
     float b_sigma;            // density bias

@@ -200,6 +200,20 @@ def _desc_of(sc, sig, uvw, beta, dec):
     return desc
 
 
+def test_linear_tune_keeps_four_lanes():
+    """The linear decoder renders with four lanes per ray only, so tuning
+    measures that one shape and keeps it."""
+    import torch
+    from paper_2204_02585_amd import binding
+    sc = _small(width=32, height=24, focal=40.0)
+    caches = binding.caches_from_scene(sc)
+    try:
+        P = torch.from_numpy(sc.poses).cuda()
+        assert caches.tune_lanes_per_ray(P, sc.intrinsics, sc.near, sc.far, sc.config.n_samples) == 4
+    finally:
+        caches.close()
+
+
 def test_linear_handle_options():
     from paper_2204_02585_amd import binding
     sc = scenes.make_scene("tiny_alt")

@@ -400,6 +400,34 @@ def test_launch_option_validation():
     assert binding.lib.sqn_set_empty_space_skipping(None, 1) == binding.SQN_ERR_INVALID_ARG
 
 
+@pytest.mark.parametrize("views", [1, 3])
+def test_tune_lanes_per_ray(views):
+    """sqn_tune_lanes_per_ray picks one of the launch shapes by timing them
+    on the batch; renders after it (one lane per ray on a single view deals
+    its tiles from the centre outwards) keep parity with the oracle."""
+    import torch
+    from paper_2204_02585_amd import binding
+    sc = _small("tiny", width=48, height=40, n_poses=views)
+    caches = binding.caches_from_scene(sc)
+    try:
+        P = torch.from_numpy(sc.poses).cuda()
+        chosen = caches.tune_lanes_per_ray(P, sc.intrinsics, sc.near, sc.far, sc.config.n_samples)
+        assert chosen in (1, 4, 8)
+        rgb, depth = caches.render(P, sc.intrinsics, sc.near, sc.far, sc.config.n_samples)
+        torch.cuda.synchronize()
+        gpu = (rgb.cpu().numpy().reshape(-1, 3), depth.cpu().numpy().reshape(-1), None)
+        ref = oracle.render_scene(sc)
+        pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), f"tuned L={chosen} views={views}")
+        # a bad batch leaves the handle as it was and reports the error
+        bad = binding.lib.sqn_tune_lanes_per_ray(caches.handle, binding._ptr(P), views, None, sc.near, sc.far,
+                                                 sc.config.n_samples, None, None, None, None)
+        assert bad == binding.SQN_ERR_INVALID_ARG
+    finally:
+        caches.close()
+    assert binding.lib.sqn_tune_lanes_per_ray(None, None, 0, None, 2.0, 6.0, 1, None, None, None,
+                                              None) == binding.SQN_ERR_INVALID_ARG
+
+
 def test_create_out_of_memory_hook(monkeypatch):
     import torch
     from paper_2204_02585_amd import binding
