@@ -78,7 +78,7 @@ def counter_record(config_name, kind="render", lanes=None):
         return None
     if rec.get(f"{kind}_hip_sha256_16") != sha:
         return None
-    if lanes and f"L={lanes}," not in rec.get("kernel", ""):
+    if lanes and (f"L={lanes}," if lanes > 0 else "hybrid") not in rec.get("kernel", ""):
         return None
     return rec
 
@@ -434,6 +434,7 @@ def main():
         print("[bench] tuning lanes per ray", file=sys.stderr, flush=True)
         lanes = caches.tune_lanes_per_ray(poses, scene.intrinsics, scene.near, scene.far, N, rgb, depth,
                                           stream=stream)
+    caches_centre = getattr(caches, "centre_block", 0.0)
 
     # untimed diagnostics pass: live / occupied sample counts for the byte model
     _, _, st = caches.render_stats(poses, scene.intrinsics, scene.near, scene.far, N)
@@ -514,8 +515,8 @@ def main():
                    "direction_cache": [cfg.n_theta, cfg.n_phi], "t_eps": cfg.t_eps,
                    "decoder": ("Eq. 5 linear, D_sigma=%d" % cfg.sigma_channels
                                if cfg.sigma_channels > 0 else "Eq. 4 product/sum"),
-                   "lanes_per_ray": (f"tuned: {lanes}" if args.lanes == 0 and not args.no_tune
-                                     else (args.lanes or "auto")),
+                   "lanes_per_ray": ((f"tuned: hybrid {caches_centre:g}" if lanes == -1 else f"tuned: {lanes}")
+                                     if args.lanes == 0 and not args.no_tune else (args.lanes or "auto")),
                    "empty_space_leaps": not args.dense},
         "frames_per_s": round(fps, 2),
         "samples": {"nominal_per_step": nominal, "live_inbox_per_step": live_inbox,

@@ -233,27 +233,46 @@ sqn_status sqn_render_stats(const sqn_caches* caches,
  * made by sqn_create_linear_caches (always four lanes). */
 sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes);
 
+/* Hybrid launch of single views: the centred rectangle of blocks of 16 x 16
+ * pixels spanning `fraction` of the image's blocks along each axis marches
+ * with four lanes per ray (its workgroups are dispatched first), every other
+ * block with one lane per ray.  The long chains of samples over a centred
+ * object then end four times sooner while the rest of the image costs a
+ * quarter of the instructions.  Applies to one view at a time on a handle
+ * from sqn_create_caches with empty-space skipping and world rays; other
+ * renders use the lanes-per-ray setting.  0 (the default) turns it off;
+ * sqn_set_lanes_per_ray also turns it off.  Sample, index and termination
+ * decisions are identical for every choice.  Not thread-safe against
+ * concurrent renders with the handle.
+ * Errors: SQN_ERR_INVALID_ARG for a fraction outside [0, 1] or a NULL
+ * handle; SQN_ERR_UNSUPPORTED for a fraction > 0 on a handle made by
+ * sqn_create_linear_caches. */
+sqn_status sqn_set_centre_block(sqn_caches* caches, float fraction);
+
 /* Measure the launch shapes on one batch and keep the fastest: renders the
- * batch (arguments as sqn_render) with 4, 1 and 8 lanes per ray (four only
- * for a handle made by sqn_create_linear_caches), each once untimed and five
- * times between two HIP events on `stream`, then sets the handle's lanes
- * per ray as sqn_set_lanes_per_ray would and, if lanes_out is not NULL,
- * writes the choice there (for an empty batch the setting stays).  No
- * candidate changes a sample, index or termination decision, only the
- * time; which is fastest depends on the image size, the number of views and
- * the scene (the chains of samples), which the default per-call choice sees
- * only through the number of rays.  A single view rendered with one lane
- * per ray deals its tiles from the centre of the image outwards (the long
- * rays over a centred object first).  rgb_out and depth_out receive a
- * render of the batch.  Blocks until the timed renders finish; creates two
- * HIP events and allocates no device memory.  Not thread-safe against
- * concurrent renders with the handle.  Errors: those of sqn_render (the
- * handle's setting is then left as it was); SQN_ERR_DEVICE if the events
+ * batch (arguments as sqn_render) with 4, 1 and 8 lanes per ray and, for a
+ * single view where sqn_set_centre_block applies, with hybrid launches of
+ * centred fractions 0.15, 0.5 and 1 (four lanes only for a handle made by
+ * sqn_create_linear_caches), each twice untimed and 20 times between two
+ * HIP events on `stream`, then keeps the fastest as sqn_set_lanes_per_ray
+ * and sqn_set_centre_block would, and writes the choice to lanes_out (the
+ * lanes per ray, or -1 for a hybrid launch) and centre_out (the hybrid
+ * fraction, 0 otherwise) where they are not NULL (for an empty batch the
+ * settings stay and nothing is written).  No candidate changes a sample, index or
+ * termination decision, only the time; which is fastest depends on the
+ * image size, the number of views and the scene (the chains of samples),
+ * which the default per-call choice sees only through the number of rays.
+ * A single view rendered with one lane per ray deals its tiles from the
+ * centre of the image outwards.  rgb_out and depth_out receive a render of
+ * the batch.  Blocks until the timed renders finish; creates two HIP events
+ * and allocates no device memory.  Not thread-safe against concurrent
+ * renders with the handle.  Errors: those of sqn_render (the handle's
+ * settings are then left as they were); SQN_ERR_DEVICE if the events
  * fail. */
 sqn_status sqn_tune_lanes_per_ray(sqn_caches* caches, const float* poses, int32_t n_poses,
                                   const sqn_intrinsics* intrinsics, float near_plane, float far_plane,
                                   int32_t n_samples, float* rgb_out, float* depth_out, void* stream,
-                                  int32_t* lanes_out);
+                                  int32_t* lanes_out, float* centre_out);
 
 /* Leaps over empty space (1, the default) or a dense march (0).  sigma is
  * the product of the three planar sigma^j (Sec. 3.2 Eq. 4), so it vanishes

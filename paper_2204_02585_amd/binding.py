@@ -19,7 +19,8 @@ SQN_OK, SQN_ERR_INVALID_ARG, SQN_ERR_OUT_OF_MEMORY, SQN_ERR_DEVICE, SQN_ERR_UNSU
 SQN_F32, SQN_F16 = 0, 1
 
 EXPORTS = ("sqn_create_caches", "sqn_create_linear_caches", "sqn_recreate_caches", "sqn_render", "sqn_render_stats",
-           "sqn_set_lanes_per_ray", "sqn_tune_lanes_per_ray", "sqn_set_empty_space_skipping", "sqn_set_ndc", "sqn_cache_device_bytes",
+           "sqn_set_lanes_per_ray", "sqn_tune_lanes_per_ray", "sqn_set_centre_block",
+           "sqn_set_empty_space_skipping", "sqn_set_ndc", "sqn_cache_device_bytes",
            "sqn_destroy", "sqn_status_string", "sqn_last_error", "sqn_create_networks",
            "sqn_generate_caches", "sqn_networks_device_bytes", "sqn_destroy_networks")
 
@@ -93,9 +94,11 @@ def _load() -> ctypes.CDLL:
                                      vp, vp, vp, vp]
     lib.sqn_set_lanes_per_ray.restype = ctypes.c_int
     lib.sqn_set_lanes_per_ray.argtypes = [vp, i32]
+    lib.sqn_set_centre_block.restype = ctypes.c_int
+    lib.sqn_set_centre_block.argtypes = [vp, f32]
     lib.sqn_tune_lanes_per_ray.restype = ctypes.c_int
     lib.sqn_tune_lanes_per_ray.argtypes = [vp, vp, i32, ctypes.POINTER(Intrinsics), f32, f32, i32, vp, vp, vp,
-                                           ctypes.POINTER(i32)]
+                                           ctypes.POINTER(i32), ctypes.POINTER(f32)]
     lib.sqn_set_empty_space_skipping.restype = ctypes.c_int
     lib.sqn_set_empty_space_skipping.argtypes = [vp, i32]
     lib.sqn_set_ndc.restype = ctypes.c_int
@@ -273,12 +276,20 @@ class Caches:
         """1, 4 or 8 lanes of a wavefront per ray, or 0 to choose per call."""
         _check(lib.sqn_set_lanes_per_ray(self.handle, int(lanes)))
 
+    def set_centre_block(self, fraction: float) -> None:
+        """Hybrid launch of single views: the centred `fraction` of the image
+        (per axis, in 16-pixel blocks) with four lanes per ray, the rest with
+        one; 0 turns it off."""
+        _check(lib.sqn_set_centre_block(self.handle, float(fraction)))
+
     def tune_lanes_per_ray(self, poses: torch.Tensor, intrinsics: dict, near: float, far: float,
                            n_samples: int, rgb_out: Optional[torch.Tensor] = None,
                            depth_out: Optional[torch.Tensor] = None, stream=None) -> int:
-        """sqn_tune_lanes_per_ray: time the lanes-per-ray choices on this
-        batch, keep the fastest for later renders and return it.  Blocks;
-        rgb_out / depth_out (allocated if not given) receive a render."""
+        """sqn_tune_lanes_per_ray: time the launch shapes on this batch, keep
+        the fastest for later renders and return it: lanes per ray, or -1 for
+        a hybrid launch, whose centre fraction is then in self.centre_block.
+        Blocks; rgb_out / depth_out (allocated if not given) receive a
+        render."""
         poses = _poses_arg(poses)
         B = poses.shape[0]
         H, W = int(intrinsics["height"]), int(intrinsics["width"])
@@ -290,10 +301,11 @@ class Caches:
         _output_arg(depth_out, (B, H, W), poses.device, "depth_out")
         _order_after_current(stream, poses, rgb_out, depth_out)
         intr = _intrinsics(intrinsics)
-        chosen = ctypes.c_int32(0)
+        chosen, centre = ctypes.c_int32(0), ctypes.c_float(0.0)
         _check(lib.sqn_tune_lanes_per_ray(self.handle, _ptr(poses), B, ctypes.byref(intr), float(near),
                                           float(far), int(n_samples), _ptr(rgb_out), _ptr(depth_out),
-                                          _stream(stream), ctypes.byref(chosen)))
+                                          _stream(stream), ctypes.byref(chosen), ctypes.byref(centre)))
+        self.centre_block = float(centre.value)
         return int(chosen.value)
 
     def set_empty_space_skipping(self, enable: bool) -> None:

@@ -7,6 +7,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <limits>
 #include <mutex>
 #include <vector>
@@ -24,6 +25,7 @@ struct sqn_caches {
     float scale[3];          // (n_p - 1) / (bmax - bmin), binary32
     int64_t tau_eps;         // floor(-ln(eps) 2^32)
     int32_t lanes;           // lanes per ray, 0 = chosen per call
+    float centre;            // > 0: hybrid launch of single views, centred block fraction
     int32_t skip;            // empty-space leaps (one lane per ray)
     float ndc_near;          // > 0: forward-facing rays in normalized device coordinates
     // linear (Eq. 5) decoder
@@ -312,6 +314,29 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
     // centre-out tile order: measured faster for one view with one lane per
     // ray (shorter tail), slower for batches of views and with 4 or 8 lanes
     p.centre_out = (p.lanes == 1 && n_poses == 1) ? 1 : 0;
+    // hybrid launch: a centred rectangle of 16 x 16 pixel blocks, `centre`
+    // of the image's blocks along each axis, with four lanes per ray and
+    // the other blocks with one (single views of the product decoder with
+    // leaps and world rays)
+    if (h->centre > 0.0f && n_poses == 1 && !h->linear && h->skip && !(h->ndc_near > 0.0f)) {
+        const int32_t bx = (in->width + 15) / 16, by = (in->height + 15) / 16;
+        const int32_t hw = std::min(bx, std::max(1, static_cast<int32_t>(lroundf(h->centre * static_cast<float>(bx)))));
+        const int32_t hh = std::min(by, std::max(1, static_cast<int32_t>(lroundf(h->centre * static_cast<float>(by)))));
+        p.hybrid = 1;
+        p.centre_out = 0;
+        p.hy_bx = bx;
+        p.hy_by = by;
+        p.hy_w = hw;
+        p.hy_h = hh;
+        p.hy_x0 = (bx - hw) / 2;
+        p.hy_y0 = (by - hh) / 2;
+        p.n_heavy = 4 * hw * hh;
+        const int64_t hgroups = static_cast<int64_t>(p.n_heavy) + static_cast<int64_t>(bx) * by
+                                - static_cast<int64_t>(hw) * hh;
+        if (hgroups > std::numeric_limits<int32_t>::max())
+            return fail(SQN_ERR_INVALID_ARG, "too many workgroups (%lld)", static_cast<long long>(hgroups));
+        p.n_groups = static_cast<int32_t>(hgroups);
+    }
 
     // the linear decoder's records hold binary32 partial sums
     const int sigma_records = h->linear ? SQN_F32 : h->desc.sigma_dtype;
@@ -1007,21 +1032,28 @@ sqn_status sqn_set_lanes_per_ray(sqn_caches* caches, int32_t lanes)
     if (caches->linear && (lanes == 1 || lanes == 8))
         return fail(SQN_ERR_UNSUPPORTED, "the linear decoder renders with four lanes per ray");
     caches->lanes = lanes;
+    caches->centre = 0.0f;
     return SQN_OK;
 }
 
 sqn_status sqn_tune_lanes_per_ray(sqn_caches* caches, const float* poses, int32_t n_poses,
                                   const sqn_intrinsics* intrinsics, float near_plane, float far_plane,
                                   int32_t n_samples, float* rgb_out, float* depth_out, void* stream,
-                                  int32_t* lanes_out)
+                                  int32_t* lanes_out, float* centre_out)
 {
     if (!caches)
         return fail(SQN_ERR_INVALID_ARG, "caches is NULL");
     const int32_t before = caches->lanes;
-    // the batch itself is checked by the first render
-    static const int32_t kCandidates[3] = {4, 1, 8};
-    const int n_cand = caches->linear ? 1 : 3;
-    constexpr int kReps = 5;
+    const float centre_before = caches->centre;
+    // the batch itself is checked by the first render; candidates: lanes
+    // per ray (centre 0), then hybrid launches of single views with centred
+    // blocks of 0.15, 0.5 and 1 of the image per axis (1: four lanes per ray
+    // everywhere, blocks dealt from the centre outwards)
+    static const int32_t kCandidates[6] = {4, 1, 8, 0, 0, 0};
+    static const float kCentre[6] = {0.0f, 0.0f, 0.0f, 0.15f, 0.5f, 1.0f};
+    const bool hybrid_ok = n_poses == 1 && !caches->linear && caches->skip && !(caches->ndc_near > 0.0f);
+    const int n_cand = caches->linear ? 1 : (hybrid_ok ? 6 : 3);
+    constexpr int kWarm = 2, kReps = 20;
     hipStream_t st = static_cast<hipStream_t>(stream);
     hipEvent_t ev[2] = {nullptr, nullptr};
     for (int k = 0; k < 2; ++k)
@@ -1032,13 +1064,15 @@ sqn_status sqn_tune_lanes_per_ray(sqn_caches* caches, const float* poses, int32_
             return fail(SQN_ERR_DEVICE, "hipEventCreate failed");
         }
     sqn_status s = SQN_OK;
-    int32_t best = kCandidates[0];
+    int best = 0;
     float best_ms = INFINITY;
     for (int c = 0; c < n_cand && s == SQN_OK; ++c) {
         caches->lanes = kCandidates[c];
-        // one untimed call (code and caches warm), then kReps timed ones
-        s = render_common(caches, poses, n_poses, intrinsics, near_plane, far_plane, n_samples, rgb_out,
-                          depth_out, nullptr, stream);
+        caches->centre = kCentre[c];
+        // kWarm untimed calls (code and caches warm), then kReps timed ones
+        for (int r = 0; r < kWarm && s == SQN_OK; ++r)
+            s = render_common(caches, poses, n_poses, intrinsics, near_plane, far_plane, n_samples, rgb_out,
+                              depth_out, nullptr, stream);
         if (s != SQN_OK || n_poses == 0)
             break;
         hipError_t e = hipEventRecord(ev[0], st);
@@ -1061,18 +1095,34 @@ sqn_status sqn_tune_lanes_per_ray(sqn_caches* caches, const float* poses, int32_
         }
         if (ms < best_ms) {
             best_ms = ms;
-            best = kCandidates[c];
+            best = c;
         }
     }
     (void)hipEventDestroy(ev[0]);
     (void)hipEventDestroy(ev[1]);
-    if (s != SQN_OK) {
+    if (s != SQN_OK || n_poses == 0) {
         caches->lanes = before;
+        caches->centre = centre_before;
         return s;
     }
-    caches->lanes = n_poses == 0 ? before : best;
+    caches->lanes = kCandidates[best];
+    caches->centre = kCentre[best];
     if (lanes_out)
-        *lanes_out = caches->lanes;
+        *lanes_out = kCentre[best] > 0.0f ? -1 : kCandidates[best];
+    if (centre_out)
+        *centre_out = kCentre[best];
+    return SQN_OK;
+}
+
+sqn_status sqn_set_centre_block(sqn_caches* caches, float fraction)
+{
+    if (!caches)
+        return fail(SQN_ERR_INVALID_ARG, "caches is NULL");
+    if (!(fraction >= 0.0f && fraction <= 1.0f))
+        return fail(SQN_ERR_INVALID_ARG, "centre block fraction %g outside [0, 1]", static_cast<double>(fraction));
+    if (caches->linear && fraction > 0.0f)
+        return fail(SQN_ERR_UNSUPPORTED, "the linear decoder renders with four lanes per ray");
+    caches->centre = fraction;
     return SQN_OK;
 }
 

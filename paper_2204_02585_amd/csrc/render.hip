@@ -1338,37 +1338,15 @@ constexpr int occupancy()
     return regs < by_lds ? regs : (by_lds < 1 ? 1 : by_lds);
 }
 
+// One workgroup's rays at tile (tx, ty) of view `view`, with the LDS arrays
+// of the launch shape: beta, the Eq. 5 rows, the colour queue and sums, and
+// (four or eight lanes) the rays' march geometry.
 template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool LIN, bool NDC>
-__global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) void render_kernel(const RenderParams P)
+__device__ __forceinline__ void workgroup_rays(const RenderParams& P, int32_t view, int32_t tx, int32_t ty,
+                                               float* beta_smem, float* lin_smem, uint4* queue_smem,
+                                               double* qacc_smem, RayGeom* geom)
 {
-    // beta of every lane's ray, component-major so that a wave-wide read of
-    // one component touches consecutive LDS words; each lane reads only what
-    // it wrote, so no barrier is needed
-    __shared__ float beta_smem[beta_smem_floats<DC, LIN, L>()];
-    // Eq. 5: one row of folded weights per ray, written and read only by
-    // the ray's own lanes
-    __shared__ __align__(16) float lin_smem[lin_smem_floats<DC, LIN>()];
-    // deferred colour: a ring of queued samples and the rays' rgb sums per wave
-    constexpr bool kDefer = defers_colour(DC, LIN);
-    __shared__ uint4 queue_smem[kDefer ? 4 * kQueue : 1];
-    __shared__ double qacc_smem[kDefer ? 4 * (64 / L) * 3 : 1];
     const int32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int32_t tile = xcd_tile_order(static_cast<int32_t>(blockIdx.x), P.n_groups);
-    const int32_t tiles_per_view = P.tiles_x * P.tiles_y;
-    const int32_t view = tile / tiles_per_view;
-    const int32_t tr = tile - view * tiles_per_view;
-    int32_t ty = tr / P.tiles_x;
-    int32_t tx = tr - ty * P.tiles_x;
-    if (P.centre_out) {
-        // one view with one lane per ray: its time is set by the waves with
-        // the longest chains of samples, which sit over the middle of the
-        // image for a centred object, so those tiles go first and the light
-        // edge tiles fill the end of the launch; k -> n/2, n/2 - 1, n/2 + 1,
-        // ... is a bijection of [0, n)
-        auto centre = [](int32_t k, int32_t n) { return (k & 1) == 0 ? n / 2 + k / 2 : n / 2 - 1 - k / 2; };
-        ty = centre(ty, P.tiles_y);
-        tx = centre(tx, P.tiles_x);
-    }
     constexpr int32_t WW = kWaveW(L), WH = kWaveH(L);
     const int32_t slot = lane / L;
     const int32_t u = tx * kTileW(L) + (wave & 1) * WW + (slot % WW);
@@ -1380,7 +1358,6 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) 
         // costs one wave's instructions per workgroup instead of L (the
         // march is bound by vector-ALU issue).  Eq. 5 (four lanes) keeps
         // beta in the ray's row of folded weights, which its lanes fold.
-        __shared__ RayGeom geom[64];
         constexpr int32_t stride = LIN && DC > 0 ? lin_stride(DC) : 0;
         auto lin_row = [&](int32_t r) { return lin_smem + r * (DC > 0 ? stride : P.lin_stride); };
         constexpr int32_t RPW = 64 / L;   // rays per wave
@@ -1425,6 +1402,138 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) 
     }
 }
 
+// k -> n/2, n/2 - 1, n/2 + 1, ...: a bijection of [0, n) that starts at the
+// middle
+__device__ __forceinline__ int32_t centre_first(int32_t k, int32_t n)
+{
+    return (k & 1) == 0 ? n / 2 + k / 2 : n / 2 - 1 - k / 2;
+}
+
+template <typename ST, typename UT, int DC, bool STATS, int L, bool SKIP, bool LIN, bool NDC>
+__global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) void render_kernel(const RenderParams P)
+{
+    // beta of every lane's ray, component-major so that a wave-wide read of
+    // one component touches consecutive LDS words; each lane reads only what
+    // it wrote, so no barrier is needed
+    __shared__ float beta_smem[beta_smem_floats<DC, LIN, L>()];
+    // Eq. 5: one row of folded weights per ray, written and read only by
+    // the ray's own lanes
+    __shared__ __align__(16) float lin_smem[lin_smem_floats<DC, LIN>()];
+    // deferred colour: a ring of queued samples and the rays' rgb sums per wave
+    constexpr bool kDefer = defers_colour(DC, LIN);
+    __shared__ uint4 queue_smem[kDefer ? 4 * kQueue : 1];
+    __shared__ double qacc_smem[kDefer ? 4 * (64 / L) * 3 : 1];
+    __shared__ RayGeom geom_smem[L >= 4 ? 64 : 1];
+    const int32_t tile = xcd_tile_order(static_cast<int32_t>(blockIdx.x), P.n_groups);
+    const int32_t tiles_per_view = P.tiles_x * P.tiles_y;
+    const int32_t view = tile / tiles_per_view;
+    const int32_t tr = tile - view * tiles_per_view;
+    int32_t ty = tr / P.tiles_x;
+    int32_t tx = tr - ty * P.tiles_x;
+    if (P.centre_out) {
+        // one view with one lane per ray: its time is set by the waves with
+        // the longest chains of samples, which sit over the middle of the
+        // image for a centred object, so those tiles go first and the light
+        // edge tiles fill the end of the launch
+        ty = centre_first(ty, P.tiles_y);
+        tx = centre_first(tx, P.tiles_x);
+    }
+    workgroup_rays<ST, UT, DC, STATS, L, SKIP, LIN, NDC>(P, view, tx, ty, beta_smem, lin_smem, queue_smem, qacc_smem,
+                                                         geom_smem);
+}
+
+// LDS bytes of one workgroup of a hybrid launch with L lanes per ray: the
+// colour queue, the rays' rgb sums, (four lanes) the march geometry, beta;
+// both shapes carve them from one buffer, 16-byte aligned.
+template <typename UT, int DC, int L>
+constexpr int hybrid_lds_bytes()
+{
+    constexpr bool defer = defers_colour(DC, false);
+    return (defer ? 4 * static_cast<int>(kQueue) * 16 : 16) + (defer ? 4 * (64 / L) * 3 * 8 : 16)
+           + (L >= 4 ? 64 * static_cast<int>(sizeof(RayGeom)) : 0) + 4 * beta_smem_floats<DC, false, L>();
+}
+
+template <typename UT, int DC>
+constexpr int hybrid_occupancy()
+{
+    constexpr int a = occupancy<UT, DC, false, false, 1>(), b = occupancy<UT, DC, false, false, 4>();
+    constexpr int bytes = hybrid_lds_bytes<UT, DC, 1>() > hybrid_lds_bytes<UT, DC, 4>()
+                              ? hybrid_lds_bytes<UT, DC, 1>()
+                              : hybrid_lds_bytes<UT, DC, 4>();
+    constexpr int by_lds = 163840 / bytes;
+    constexpr int m = a < b ? a : b;
+    return m < by_lds ? m : by_lds;
+}
+
+// One view, leaps, world rays, Eq. 4.  The image is cut into blocks of 16 x
+// 16 pixels (one workgroup of one lane per ray, four of four lanes); the
+// first n_heavy workgroups march a centred rectangle of hy_w x hy_h blocks
+// with four lanes per ray (the long chains of samples over a centred object
+// become four times shorter), the others march every other block with one
+// lane per ray (a quarter of the instructions).  Workgroups are either kind
+// as a whole, so the barrier of the four-lane setup is taken by all or none
+// of a workgroup's waves.
+template <typename ST, typename UT, int DC, bool STATS>
+__global__ __launch_bounds__(kBlockThreads, (hybrid_occupancy<UT, DC>())) void render_kernel_hybrid(
+    const RenderParams P)
+{
+    constexpr bool kDefer = defers_colour(DC, false);
+    constexpr int kQ = kDefer ? 4 * static_cast<int>(kQueue) * 16 : 16;
+    constexpr int kBytes = hybrid_lds_bytes<UT, DC, 1>() > hybrid_lds_bytes<UT, DC, 4>()
+                               ? hybrid_lds_bytes<UT, DC, 1>()
+                               : hybrid_lds_bytes<UT, DC, 4>();
+    __shared__ __align__(16) unsigned char lds[kBytes];
+    uint4* queue = reinterpret_cast<uint4*>(lds);
+    const int32_t bid = static_cast<int32_t>(blockIdx.x);
+    if (bid < P.n_heavy) {
+        // four workgroups (8 x 8 pixels each) per block; blocks from the
+        // middle of the rectangle outwards
+        constexpr int kAcc = kDefer ? 4 * 16 * 3 * 8 : 16;
+        double* acc = reinterpret_cast<double*>(lds + kQ);
+        RayGeom* geom = reinterpret_cast<RayGeom*>(lds + kQ + kAcc);
+        float* beta = reinterpret_cast<float*>(lds + kQ + kAcc + 64 * sizeof(RayGeom));
+        const int32_t blk = bid >> 2, sub = bid & 3;
+        const int32_t by = P.hy_y0 + centre_first(blk / P.hy_w, P.hy_h);
+        const int32_t bx = P.hy_x0 + centre_first(blk % P.hy_w, P.hy_w);
+        workgroup_rays<ST, UT, DC, STATS, 4, true, false, false>(P, 0, 2 * bx + (sub & 1), 2 * by + (sub >> 1), beta,
+                                                                 nullptr, queue, acc, geom);
+    } else {
+        // the blocks outside the rectangle, row by row: the rows above it,
+        // the rows beside it (left part, then right part), the rows below
+        constexpr int kAcc = kDefer ? 4 * 64 * 3 * 8 : 16;
+        double* acc = reinterpret_cast<double*>(lds + kQ);
+        float* beta = reinterpret_cast<float*>(lds + kQ + kAcc);
+        int32_t l = bid - P.n_heavy, bx, by;
+        const int32_t above = P.hy_y0 * P.hy_bx, side = P.hy_bx - P.hy_w;
+        if (l < above) {
+            by = l / P.hy_bx;
+            bx = l - by * P.hy_bx;
+        } else if ((l -= above) < P.hy_h * side) {
+            const int32_t r = l / side, k = l - r * side;
+            by = P.hy_y0 + r;
+            bx = k < P.hy_x0 ? k : k + P.hy_w;
+        } else {
+            l -= P.hy_h * side;
+            const int32_t r = l / P.hy_bx;
+            by = P.hy_y0 + P.hy_h + r;
+            bx = l - r * P.hy_bx;
+        }
+        workgroup_rays<ST, UT, DC, STATS, 1, true, false, false>(P, 0, bx, by, beta, nullptr, queue, acc, nullptr);
+    }
+}
+
+template <typename ST, typename UT, int DC>
+hipError_t launch_hybrid(const RenderParams& p, bool stats, hipStream_t stream)
+{
+    const dim3 grid(static_cast<uint32_t>(p.n_groups));
+    const dim3 block(kBlockThreads);
+    if (stats)
+        render_kernel_hybrid<ST, UT, DC, true><<<grid, block, 0, stream>>>(p);
+    else
+        render_kernel_hybrid<ST, UT, DC, false><<<grid, block, 0, stream>>>(p);
+    return hipGetLastError();
+}
+
 template <typename ST, typename UT, int DC, int L, bool SKIP, bool LIN, bool NDC>
 hipError_t launch_ray_space(const RenderParams& p, bool stats, hipStream_t stream)
 {
@@ -1448,6 +1557,8 @@ hipError_t launch_shape(const RenderParams& p, bool stats, hipStream_t stream)
 template <typename ST, typename UT, int DC>
 hipError_t launch_typed(const RenderParams& p, bool stats, hipStream_t stream)
 {
+    if (p.hybrid)
+        return launch_hybrid<ST, UT, DC>(p, stats, stream);
     if (p.lanes == 1)
         return p.skip ? launch_shape<ST, UT, DC, 1, true, false>(p, stats, stream)
                       : launch_shape<ST, UT, DC, 1, false, false>(p, stats, stream);

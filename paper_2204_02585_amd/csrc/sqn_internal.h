@@ -48,6 +48,13 @@ struct RenderParams {
     int32_t tiles_x, tiles_y; // workgroup tiles per view
     int32_t n_groups;         // workgroups in the grid
     int32_t centre_out;       // 1: tile rows and columns dealt from the image centre outwards
+    // hybrid launch (one view): a centred rectangle of blocks of 16 x 16
+    // pixels marched with four lanes per ray, the other blocks with one
+    int32_t hybrid;           // 1: hybrid launch
+    int32_t hy_bx, hy_by;     // blocks per image row and column
+    int32_t hy_x0, hy_y0;     // first block of the rectangle
+    int32_t hy_w, hy_h;       // rectangle size in blocks
+    int32_t n_heavy;          // workgroups of the rectangle (four per block), dispatched first
     // linear (Eq. 5) decoder; sigma[j] then holds per-plane partial sums
     int32_t linear;           // 1: Eq. 5, 0: Eq. 4
     float b_sigma;            // density bias

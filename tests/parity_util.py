@@ -18,8 +18,11 @@ def scene_atol(scene):
 
 
 # launch variants: library default (leaps, lanes chosen per call), leaps with
-# 1, 4 or 8 lanes per ray, and the dense march with 1, 4 or 8 lanes per ray
-MODES = {"auto": (0, True), "skip1": (1, True), "skip4": (4, True), "skip8": (8, True),
+# 1, 4 or 8 lanes per ray, the hybrid launch (leaps; single views of the
+# product decoder: the centred half of the image with four lanes per ray, the
+# rest with one; other renders as "auto"), and the dense march with 1, 4 or 8
+# lanes per ray
+MODES = {"auto": (0, True), "skip1": (1, True), "skip4": (4, True), "skip8": (8, True), "hyb": (0, True, 0.5),
          "L1": (1, False), "L4": (4, False), "L8": (8, False)}
 
 
@@ -29,10 +32,13 @@ def gpu_render(scene, t_eps=None, poses=None, n_samples=None, stats=True, mode="
     import torch
     from paper_2204_02585_amd import binding
     caches = binding.caches_from_scene(scene, t_eps=t_eps)
-    lanes, skip = MODES[mode]
+    lanes, skip = MODES[mode][:2]
+    centre = MODES[mode][2] if len(MODES[mode]) > 2 else 0.0
     print(f"[render {scene.config.name} {scene.config.width}x{scene.config.height}"
           f"x{scene.config.n_poses} mode={mode}]", flush=True)
     caches.set_lanes_per_ray(lanes)
+    if centre > 0.0 and scene.config.sigma_channels == 0:
+        caches.set_centre_block(centre)
     caches.set_empty_space_skipping(skip)
     P = torch.from_numpy(scene.poses if poses is None else poses).cuda()
     N = scene.config.n_samples if n_samples is None else n_samples

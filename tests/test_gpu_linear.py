@@ -210,6 +210,9 @@ def test_linear_tune_keeps_four_lanes():
     try:
         P = torch.from_numpy(sc.poses).cuda()
         assert caches.tune_lanes_per_ray(P, sc.intrinsics, sc.near, sc.far, sc.config.n_samples) == 4
+        with pytest.raises(binding.SqnError):
+            caches.set_centre_block(0.5)
+        caches.set_centre_block(0.0)
     finally:
         caches.close()
 

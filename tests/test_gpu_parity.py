@@ -400,6 +400,34 @@ def test_launch_option_validation():
     assert binding.lib.sqn_set_empty_space_skipping(None, 1) == binding.SQN_ERR_INVALID_ARG
 
 
+@pytest.mark.parametrize("fraction", [0.15, 0.5, 1.0])
+@pytest.mark.parametrize("W,H", [(1, 1), (37, 23), (16, 16), (70, 33), (64, 64)])
+def test_hybrid_launch_fractions(W, H, fraction):
+    """Hybrid launches: the centred rectangle of 16-pixel blocks with four
+    lanes per ray (all of the image at fraction 1), the rest with one, at
+    ragged image sizes; the stats variant renders the same values."""
+    import torch
+    from paper_2204_02585_amd import binding
+    sc = _small("tiny", width=W, height=H, focal=1.25 * max(W, H))
+    caches = binding.caches_from_scene(sc)
+    try:
+        caches.set_centre_block(fraction)
+        P = torch.from_numpy(sc.poses).cuda()
+        rgb, depth, st = caches.render_stats(P, sc.intrinsics, sc.near, sc.far, sc.config.n_samples)
+        rgb2, depth2 = caches.render(P, sc.intrinsics, sc.near, sc.far, sc.config.n_samples)
+        torch.cuda.synchronize()
+        assert torch.equal(rgb, rgb2) and torch.equal(depth, depth2)
+        gpu = (rgb2.cpu().numpy().reshape(-1, 3), depth2.cpu().numpy().reshape(-1),
+               st.cpu().numpy().view(np.uint32).reshape(-1, 4))
+        ref = oracle.render_scene(sc)
+        pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), f"hybrid {fraction} {W}x{H}")
+        for bad in (-0.1, 1.5, float("nan")):
+            with pytest.raises(binding.SqnError):
+                caches.set_centre_block(bad)
+    finally:
+        caches.close()
+
+
 @pytest.mark.parametrize("views", [1, 3])
 def test_tune_lanes_per_ray(views):
     """sqn_tune_lanes_per_ray picks one of the launch shapes by timing them
@@ -412,7 +440,7 @@ def test_tune_lanes_per_ray(views):
     try:
         P = torch.from_numpy(sc.poses).cuda()
         chosen = caches.tune_lanes_per_ray(P, sc.intrinsics, sc.near, sc.far, sc.config.n_samples)
-        assert chosen in (1, 4, 8)
+        assert chosen in ((-1, 1, 4, 8) if views == 1 else (1, 4, 8))
         rgb, depth = caches.render(P, sc.intrinsics, sc.near, sc.far, sc.config.n_samples)
         torch.cuda.synchronize()
         gpu = (rgb.cpu().numpy().reshape(-1, 3), depth.cpu().numpy().reshape(-1), None)
@@ -420,12 +448,12 @@ def test_tune_lanes_per_ray(views):
         pu.compare(gpu, ref, np.arange(ref.size), pu.scene_atol(sc), f"tuned L={chosen} views={views}")
         # a bad batch leaves the handle as it was and reports the error
         bad = binding.lib.sqn_tune_lanes_per_ray(caches.handle, binding._ptr(P), views, None, sc.near, sc.far,
-                                                 sc.config.n_samples, None, None, None, None)
+                                                 sc.config.n_samples, None, None, None, None, None)
         assert bad == binding.SQN_ERR_INVALID_ARG
     finally:
         caches.close()
     assert binding.lib.sqn_tune_lanes_per_ray(None, None, 0, None, 2.0, 6.0, 1, None, None, None,
-                                              None) == binding.SQN_ERR_INVALID_ARG
+                                              None, None) == binding.SQN_ERR_INVALID_ARG
 
 
 def test_create_out_of_memory_hook(monkeypatch):
