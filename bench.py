@@ -396,6 +396,8 @@ def main():
     ap.add_argument("--centre", type=float, default=0.0,
                     help="hybrid launch of a single view: centred fraction of 16-pixel blocks with four lanes per "
                          "ray (sqn_set_centre_block); 0 = off")
+    ap.add_argument("--settle", type=float, default=0.1,
+                    help="seconds of untimed rendering before the warm-up steps (the GPU clocks settle)")
     ap.add_argument("--tune", action="store_true",
                     help="time the launch shapes with sqn_tune_lanes_per_ray instead of the workload's recorded one")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -468,7 +470,17 @@ def main():
     n_rays = B * cfg.width * cfg.height
     bytes_alg = algorithmic_bytes(cfg, n_rays, live_inbox, occupied)
 
-    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    # the GPU's clocks take tens of milliseconds of load to settle after the
+    # process starts (the same launch runs up to 8% slower at first): render
+    # for args.settle seconds, untimed, before the warm-up steps
+    print(f"[bench] settle {args.settle} s, warmup {args.warmup}", file=sys.stderr, flush=True)
+    settle0 = time.perf_counter()
+    settle_calls = 0
+    while time.perf_counter() - settle0 < args.settle:
+        for _ in range(4):
+            caches.render(poses, scene.intrinsics, scene.near, scene.far, N, rgb, depth, stream=stream)
+        settle_calls += 4
+        torch.cuda.synchronize()
     for _ in range(args.warmup):
         caches.render(poses, scene.intrinsics, scene.near, scene.far, N, rgb, depth, stream=stream)
     torch.cuda.synchronize()
@@ -525,6 +537,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle": {"seconds": args.settle, "renders": settle_calls},
         "ms_per_step": round(ms, 5),
         "ms_per_launch": spread,
         "higher_is_better": True,
