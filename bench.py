@@ -307,7 +307,15 @@ def bench_generate(args):
     def step():
         nets.generate(cfg.n_p, cfg.n_theta, cfg.n_phi, g.bbox_min, g.bbox_max, out=out, stream=stream)
 
-    print(f"[bench] {cfg.name}: warmup {args.warmup}", file=sys.stderr, flush=True)
+    # untimed settle of the GPU clocks (as for the render workloads), then
+    # the warm-up steps
+    print(f"[bench] {cfg.name}: settle {args.settle} s, warmup {args.warmup}", file=sys.stderr, flush=True)
+    settle0 = time.perf_counter()
+    settle_calls = 0
+    while time.perf_counter() - settle0 < args.settle:
+        step()
+        settle_calls += 1
+        torch.cuda.synchronize()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -361,6 +369,7 @@ def bench_generate(args):
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle": {"seconds": args.settle, "calls": settle_calls},
         "ms_per_step": round(ms, 4),
         "higher_is_better": True,
         "scaling": "weak",
