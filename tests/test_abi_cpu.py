@@ -127,9 +127,9 @@ def test_linear_decoder_validation_before_device_calls(lib):
 
 
 def test_probe_library_exports_and_rejects_bad_sizes():
-    """The benchmark's ceiling probes (libsqn_probe.so: memory levels and
-    matrix cores) load and reject sizes they cannot measure before touching
-    the device."""
+    """The benchmark's ceiling probes (libsqn_probe.so: memory levels, the
+    vector-memory data path and matrix cores) load and reject sizes they
+    cannot measure before touching the device."""
     from paper_2204_02585_amd import build
     raw = ctypes.CDLL(build.PROBE_PATH)
     raw.sqn_probe_stream.argtypes = [ctypes.c_uint64, ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
@@ -144,3 +144,10 @@ def test_probe_library_exports_and_rejects_bad_sizes():
     raw.sqn_probe_mfma_f16.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
     assert raw.sqn_probe_mfma_f16(0, ctypes.byref(ms)) == 1
     assert raw.sqn_probe_mfma_f16(10, None) == 1
+    raw.sqn_probe_vmem.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_double,
+                                   ctypes.POINTER(ctypes.c_float)]
+    assert raw.sqn_probe_vmem(2, 0, 16, 2.4, ctypes.byref(ms)) == 1
+    assert raw.sqn_probe_vmem(0, 2, 16, 2.4, ctypes.byref(ms)) == 1
+    assert raw.sqn_probe_vmem(0, 0, 0, 2.4, ctypes.byref(ms)) == 1
+    assert raw.sqn_probe_vmem(0, 0, 16, 0.0, ctypes.byref(ms)) == 1
+    assert raw.sqn_probe_vmem(0, 0, 16, 2.4, None) == 1
