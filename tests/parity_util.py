@@ -26,16 +26,19 @@ MODES = {"auto": (0, True), "skip1": (1, True), "skip4": (4, True), "skip8": (8,
          "L1": (1, False), "L4": (4, False), "L8": (8, False)}
 
 
-def gpu_render(scene, t_eps=None, poses=None, n_samples=None, stats=True, mode="auto"):
-    """Render a scene through the C ABI in one of MODES; returns numpy
-    (rgb, depth, stats)."""
+def gpu_render(scene, t_eps=None, poses=None, n_samples=None, stats=True, mode="auto", shape=None):
+    """Render a scene through the C ABI in one of MODES, or in an explicit
+    launch shape (lanes per ray, hybrid centre fraction) with leaps; returns
+    numpy (rgb, depth, stats)."""
     import torch
     from paper_2204_02585_amd import binding
     caches = binding.caches_from_scene(scene, t_eps=t_eps)
     lanes, skip = MODES[mode][:2]
     centre = MODES[mode][2] if len(MODES[mode]) > 2 else 0.0
+    if shape is not None:
+        (lanes, centre), skip = shape, True
     print(f"[render {scene.config.name} {scene.config.width}x{scene.config.height}"
-          f"x{scene.config.n_poses} mode={mode}]", flush=True)
+          f"x{scene.config.n_poses} mode={mode if shape is None else shape}]", flush=True)
     caches.set_lanes_per_ray(lanes)
     if centre > 0.0 and scene.config.sigma_channels == 0:
         caches.set_centre_block(centre)

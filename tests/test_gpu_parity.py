@@ -284,6 +284,21 @@ def test_full_size_stress(mode):
     pu.compare(gpu, ref, ids, pu.scene_atol(sc), "stress")
 
 
+@pytest.mark.parametrize("name,n_random", [("paper", 40000), ("large", 30000), ("paper512", 30000),
+                                           ("stress", 20000), ("batch", 20000), ("llff", 20000)])
+def test_full_size_recorded_launch_shapes(name, n_random):
+    """Each workload in the launch shape bench.py times it in (its
+    LAUNCH_SHAPES entry), sampled rays against the oracle."""
+    import bench
+    sc = scenes.make_scene(name)
+    cfg = sc.config
+    shape = bench.LAUNCH_SHAPES[name]
+    gpu = pu.gpu_render(sc, shape=shape)
+    ids = pu.sample_ray_ids(cfg.n_poses, cfg.height, cfg.width, n_random, seed=cfg.number)
+    ref = oracle.render_scene(sc, ray_ids=ids)
+    pu.compare(gpu, ref, ids, pu.scene_atol(sc), f"{name} shape {shape}")
+
+
 # ------------------------------------------------------------ C-ABI errors
 
 def test_abi_rejects_bad_arguments():
