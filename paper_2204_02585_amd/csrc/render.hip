@@ -1492,7 +1492,15 @@ __global__ __launch_bounds__(kBlockThreads, (hybrid_occupancy<UT, DC>())) void r
         double* acc = reinterpret_cast<double*>(lds + kQ);
         RayGeom* geom = reinterpret_cast<RayGeom*>(lds + kQ + kAcc);
         float* beta = reinterpret_cast<float*>(lds + kQ + kAcc + 64 * sizeof(RayGeom));
-        const int32_t blk = bid >> 2, sub = bid & 3;
+        // consecutive workgroups go to the 8 XCDs in turn: the four of a
+        // block are the ones 8 apart, so they share one XCD's L2 (a full
+        // group of 8 blocks at a time; the last partial group in order)
+        int32_t blk = bid >> 2, sub = bid & 3;
+        if (bid < (P.n_heavy & ~31)) {
+            const int32_t xcd = bid & 7, li = bid >> 3;
+            blk = 8 * (li >> 2) + xcd;
+            sub = li & 3;
+        }
         const int32_t by = P.hy_y0 + centre_first(blk / P.hy_w, P.hy_h);
         const int32_t bx = P.hy_x0 + centre_first(blk % P.hy_w, P.hy_w);
         workgroup_rays<ST, UT, DC, STATS, 4, true, false, false>(P, 0, 2 * bx + (sub & 1), 2 * by + (sub >> 1), beta,
