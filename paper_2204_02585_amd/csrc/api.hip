@@ -312,8 +312,19 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
         return fail(SQN_ERR_INVALID_ARG, "too many workgroups (%lld)", static_cast<long long>(groups));
     p.n_groups = static_cast<int32_t>(groups);
     // centre-out tile order: measured faster for one view with one lane per
-    // ray (shorter tail), slower for batches of views and with 4 or 8 lanes
+    // ray (shorter tail); batches of views keep the plain order
     p.centre_out = (p.lanes == 1 && n_poses == 1) ? 1 : 0;
+    // one view with four or eight lanes per ray: blocks of 2 x 2 tiles from
+    // the centre outwards, each block's four workgroups on one XCD so that
+    // its L2 serves the texels they share (measured 2-4% faster than tiles in
+    // row order); the grid covers whole blocks
+    if (p.lanes >= 4 && n_poses == 1) {
+        const int64_t bgroups = 4 * ((static_cast<int64_t>(p.tiles_x) + 1) / 2) * ((p.tiles_y + 1) / 2);
+        if (bgroups > std::numeric_limits<int32_t>::max())
+            return fail(SQN_ERR_INVALID_ARG, "too many workgroups (%lld)", static_cast<long long>(bgroups));
+        p.block_order = 1;
+        p.n_groups = static_cast<int32_t>(bgroups);
+    }
     // hybrid launch: a centred rectangle of 16 x 16 pixel blocks, `centre`
     // of the image's blocks along each axis, with four lanes per ray and
     // the other blocks with one (single views of the product decoder with

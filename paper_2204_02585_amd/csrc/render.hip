@@ -1424,12 +1424,31 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) 
     __shared__ uint4 queue_smem[kDefer ? 4 * kQueue : 1];
     __shared__ double qacc_smem[kDefer ? 4 * (64 / L) * 3 : 1];
     __shared__ RayGeom geom_smem[L >= 4 ? 64 : 1];
-    const int32_t tile = xcd_tile_order(static_cast<int32_t>(blockIdx.x), P.n_groups);
-    const int32_t tiles_per_view = P.tiles_x * P.tiles_y;
-    const int32_t view = tile / tiles_per_view;
-    const int32_t tr = tile - view * tiles_per_view;
-    int32_t ty = tr / P.tiles_x;
-    int32_t tx = tr - ty * P.tiles_x;
+    int32_t view, tx, ty;
+    if (P.block_order) {
+        // one view: blocks of 2 x 2 tiles from the centre outwards, the
+        // four workgroups of a block the ones 8 apart in dispatch order (one
+        // XCD, whose L2 then holds their shared texels); the grid covers
+        // whole blocks, and tiles past the image edge render nothing
+        const int32_t bx = (P.tiles_x + 1) >> 1, by = (P.tiles_y + 1) >> 1;
+        const int32_t bid = static_cast<int32_t>(blockIdx.x);
+        int32_t blk = bid >> 2, sub = bid & 3;
+        if (bid < (P.n_groups & ~31)) {
+            const int32_t li = bid >> 3;
+            blk = 8 * (li >> 2) + (bid & 7);
+            sub = li & 3;
+        }
+        view = 0;
+        tx = 2 * centre_first(blk % bx, bx) + (sub & 1);
+        ty = 2 * centre_first(blk / bx, by) + (sub >> 1);
+    } else {
+        const int32_t tile = xcd_tile_order(static_cast<int32_t>(blockIdx.x), P.n_groups);
+        const int32_t tiles_per_view = P.tiles_x * P.tiles_y;
+        view = tile / tiles_per_view;
+        const int32_t tr = tile - view * tiles_per_view;
+        ty = tr / P.tiles_x;
+        tx = tr - ty * P.tiles_x;
+    }
     if (P.centre_out) {
         // one view with one lane per ray: its time is set by the waves with
         // the longest chains of samples, which sit over the middle of the
