@@ -415,6 +415,9 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--vmem-probe", action="store_true",
                     help="only run the vector-memory saturation probe and print its cycles per load")
+    ap.add_argument("--graph", type=int, default=0,
+                    help="also time a serving loop that replays a HIP graph of this many captured renders "
+                         "(reported as graph_replay, beside the eager figures; 0 = off)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB device-to-device 3 times (a kernel "
                          "of known traffic for scaling hardware byte counters)")
@@ -518,6 +521,10 @@ def main():
     per = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
     spread = {"median": round(per[len(per) // 2], 5), "min": round(per[0], 5), "max": round(per[-1], 5)}
 
+    graph_replay = None
+    if args.graph > 0:
+        graph_replay = time_graph_replay(caches, poses, scene, N, rgb, depth, args.graph, args.steps, ms)
+
     nominal = cfg.nominal_samples
     msps = nominal / (ms * 1e-3) / 1e6
     fps = B / (ms * 1e-3)
@@ -574,7 +581,44 @@ def main():
         "ceilings": ceilings,
         "wall_s_timed": round(wall, 4),
     }
+    if graph_replay is not None:
+        out["graph_replay"] = graph_replay
     print(json.dumps(out), flush=True)
+
+
+def time_graph_replay(caches, poses, scene, N, rgb, depth, per_graph, steps, eager_ms):
+    """A serving loop's launch pattern: `per_graph` renders captured once in
+    a HIP graph (torch.cuda.CUDAGraph; the renders allocate nothing and
+    issue no memset), the graph replayed until about `steps` renders ran,
+    between two HIP events.  Outside the timed region of `value`."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        caches.render(poses, scene.intrinsics, scene.near, scene.far, N, rgb, depth)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(per_graph):
+            caches.render(poses, scene.intrinsics, scene.near, scene.far, N, rgb, depth)
+    reps = max(1, steps // per_graph)
+    for _ in range(2):
+        g.replay()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(reps):
+        g.replay()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / (reps * per_graph)
+    del g
+    return {"renders_per_graph": per_graph, "renders_timed": reps * per_graph,
+            "ms_per_render": round(ms, 5), "eager_ms_per_render": round(eager_ms, 5),
+            "eager_over_graph": round(eager_ms / ms, 3)}
 
 
 if __name__ == "__main__":
