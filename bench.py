@@ -194,17 +194,22 @@ def memory_ceilings(cache_bytes):
     """Ceilings of the memory levels the render kernel's gathers are served
     from, measured on this GPU by libsqn_probe.so: streaming reads of a
     2 MiB buffer (held by each XCD's L2), a 128 MiB buffer (held by the
-    MALL) and a 4 GiB buffer (HBM), and random 64-byte-record gathers over
+    MALL) and a 4 GiB buffer (HBM; also with non-temporal loads, the
+    streaming ceiling of HBM), and random 64-byte-record gathers over
     buffers of those sizes and of the workload's cache size.  GB/s."""
     import ctypes
     from paper_2204_02585_amd import build as _build
     lib = ctypes.CDLL(_build.PROBE_PATH)
     lib.sqn_probe_stream.argtypes = [ctypes.c_uint64, ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
+    lib.sqn_probe_stream_nt.argtypes = lib.sqn_probe_stream.argtypes
     lib.sqn_probe_gather.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.POINTER(ctypes.c_float)]
     ms = ctypes.c_float()
     out = {"stream_gbs": {}, "gather64_gbs": {}}
-    for label, nbytes, passes in (("2MiB", 2 << 20, 2000), ("128MiB", 128 << 20, 16), ("4GiB", 4 << 30, 1)):
-        if lib.sqn_probe_stream(nbytes, passes, ctypes.byref(ms)) != 0:
+    for label, nbytes, passes, probe in (("2MiB", 2 << 20, 2000, lib.sqn_probe_stream),
+                                         ("128MiB", 128 << 20, 16, lib.sqn_probe_stream),
+                                         ("4GiB", 4 << 30, 1, lib.sqn_probe_stream),
+                                         ("4GiB_nontemporal", 4 << 30, 1, lib.sqn_probe_stream_nt)):
+        if probe(nbytes, passes, ctypes.byref(ms)) != 0:
             raise RuntimeError("stream probe failed")
         out["stream_gbs"][label] = round(nbytes * passes / (ms.value * 1e-3) / 1e9, 1)
     cache_label = f"cache {cache_bytes / 1e6:.1f} MB"

@@ -138,6 +138,9 @@ def test_probe_library_exports_and_rejects_bad_sizes():
     assert raw.sqn_probe_stream(15, 1, ctypes.byref(ms)) == 1
     assert raw.sqn_probe_stream(1 << 20, 0, ctypes.byref(ms)) == 1
     assert raw.sqn_probe_stream(1 << 20, 1, None) == 1
+    raw.sqn_probe_stream_nt.argtypes = raw.sqn_probe_stream.argtypes
+    assert raw.sqn_probe_stream_nt(15, 1, ctypes.byref(ms)) == 1
+    assert raw.sqn_probe_stream_nt(1 << 20, 0, ctypes.byref(ms)) == 1
     assert raw.sqn_probe_gather(100, 1, ctypes.byref(ms)) == 1
     assert raw.sqn_probe_gather(1 << 20, 0, ctypes.byref(ms)) == 1
     assert raw.sqn_probe_gather(64 << 32, 1, ctypes.byref(ms)) == 1
