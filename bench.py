@@ -168,24 +168,28 @@ def baseline_threads():
 
 def cpu_baseline(scene, budget_s=12.0, max_frames=40):
     """The CPU oracle as it stands, on whole frames of the same workload,
-    repeated until ~budget_s of wall time (at least one frame).  Threads:
-    every CPU the process may use, capped at the host's CPU share for one
-    GPU (HOST_CPU_SHARE)."""
+    repeated until ~budget_s of wall time (at least one frame): view 0 of a
+    single view, every 10th view of a batch in turn (views differ in cost).
+    Threads: every CPU the process may use, capped at the host's CPU share
+    for one GPU (HOST_CPU_SHARE)."""
     import oracle
     host = host_description()
     threads = baseline_threads()
     cfg = scene.config
+    views = list(range(0, scene.poses.shape[0], 10))
     frames = 0
     t0 = time.perf_counter()
     while True:
-        oracle.render_scene(scene, poses=scene.poses[:1], n_threads=threads)
+        v = views[frames % len(views)]
+        oracle.render_scene(scene, poses=scene.poses[v:v + 1], n_threads=threads)
         frames += 1
         el = time.perf_counter() - t0
         if el >= budget_s or frames >= max_frames:
             break
     samples = frames * cfg.width * cfg.height * cfg.n_samples
+    which = "view 0" if len(views) == 1 else f"views {', '.join(map(str, views))} in turn"
     return {"value": samples / el / 1e6, "unit": "Msamples/s", "cores": threads, "kind": "oracle",
-            "sample": f"{frames} full {cfg.width}x{cfg.height}x{cfg.n_samples} frame(s) of view 0, "
+            "sample": f"{frames} full {cfg.width}x{cfg.height}x{cfg.n_samples} frame(s) of {which}, "
                       f"{el:.1f} s wall", "frames_per_s": frames / el,
             "threads": threads, "thread_cap": HOST_CPU_SHARE, **host}
 
