@@ -253,8 +253,11 @@ sqn_status sqn_set_centre_block(sqn_caches* caches, float fraction);
  * batch (arguments as sqn_render) with 4, 1 and 8 lanes per ray and, for a
  * single view where sqn_set_centre_block applies, with hybrid launches of
  * centred fractions 0.15, 0.5 and 1 (four lanes only for a handle made by
- * sqn_create_linear_caches), each twice untimed and 20 times between two
- * HIP events on `stream`, then keeps the fastest as sqn_set_lanes_per_ray
+ * sqn_create_linear_caches): each twice untimed, then in four rounds that
+ * each render every candidate once untimed and 5 times between two HIP
+ * events on `stream` (the rounds spread the drift of the GPU's clocks as
+ * they settle over all candidates), then keeps the fastest (least total
+ * time) as sqn_set_lanes_per_ray
  * and sqn_set_centre_block would, and writes the choice to lanes_out (the
  * lanes per ray, or -1 for a hybrid launch) and centre_out (the hybrid
  * fraction, 0 otherwise) where they are not NULL (for an empty batch the
@@ -262,8 +265,8 @@ sqn_status sqn_set_centre_block(sqn_caches* caches, float fraction);
  * termination decision, only the time; which is fastest depends on the
  * image size, the number of views and the scene (the chains of samples),
  * which the default per-call choice sees only through the number of rays.
- * A single view rendered with one lane per ray deals its tiles from the
- * centre of the image outwards.  rgb_out and depth_out receive a render of
+ * A single view deals its tiles in blocks of 2 x 2 from the centre of the
+ * image outwards.  rgb_out and depth_out receive a render of
  * the batch.  Blocks until the timed renders finish; creates two HIP events
  * and allocates no device memory.  Not thread-safe against concurrent
  * renders with the handle.  Errors: those of sqn_render (the handle's

@@ -311,14 +311,15 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
     if (groups > std::numeric_limits<int32_t>::max())
         return fail(SQN_ERR_INVALID_ARG, "too many workgroups (%lld)", static_cast<long long>(groups));
     p.n_groups = static_cast<int32_t>(groups);
-    // centre-out tile order: measured faster for one view with one lane per
-    // ray (shorter tail); batches of views keep the plain order
-    p.centre_out = (p.lanes == 1 && n_poses == 1) ? 1 : 0;
-    // one view with four or eight lanes per ray: blocks of 2 x 2 tiles from
-    // the centre outwards, each block's four workgroups on one XCD so that
-    // its L2 serves the texels they share (measured 2-4% faster than tiles in
-    // row order); the grid covers whole blocks
-    if (p.lanes >= 4 && n_poses == 1) {
+    // one view: blocks of 2 x 2 tiles from the centre outwards, each block's
+    // four workgroups on one XCD so that its L2 serves the texels they share;
+    // the grid covers whole blocks.  Measured with four or eight lanes per
+    // ray against tiles in interleaved row order: 2-4% faster; with one lane
+    // against tile rows and columns dealt from the centre: 3% faster on the
+    // 800x800 view of the 256 cache, 10% on the 1K cache, 3% slower on the
+    // 512 cache at 256 samples.  Batches of views keep the interleaved row
+    // order, which spreads every view over the XCDs.
+    if (n_poses == 1) {
         const int64_t bgroups = 4 * ((static_cast<int64_t>(p.tiles_x) + 1) / 2) * ((p.tiles_y + 1) / 2);
         if (bgroups > std::numeric_limits<int32_t>::max())
             return fail(SQN_ERR_INVALID_ARG, "too many workgroups (%lld)", static_cast<long long>(bgroups));
@@ -334,7 +335,6 @@ sqn_status render_common(const sqn_caches* h, const float* poses, int32_t n_pose
         const int32_t hw = std::min(bx, std::max(1, static_cast<int32_t>(lroundf(h->centre * static_cast<float>(bx)))));
         const int32_t hh = std::min(by, std::max(1, static_cast<int32_t>(lroundf(h->centre * static_cast<float>(by)))));
         p.hybrid = 1;
-        p.centre_out = 0;
         p.hy_bx = bx;
         p.hy_by = by;
         p.hy_w = hw;
@@ -1064,7 +1064,12 @@ sqn_status sqn_tune_lanes_per_ray(sqn_caches* caches, const float* poses, int32_
     static const float kCentre[6] = {0.0f, 0.0f, 0.0f, 0.15f, 0.5f, 1.0f};
     const bool hybrid_ok = n_poses == 1 && !caches->linear && caches->skip && !(caches->ndc_near > 0.0f);
     const int n_cand = caches->linear ? 1 : (hybrid_ok ? 6 : 3);
-    constexpr int kWarm = 2, kReps = 20;
+    // every candidate twice untimed (code and caches warm), then kRounds
+    // rounds that each time every candidate over kReps renders (after one
+    // untimed render in its shape): the GPU's clocks settle over the first
+    // tens of milliseconds of load, and rounds spread that drift over all
+    // candidates instead of favouring the last ones
+    constexpr int kWarm = 2, kRounds = 4, kReps = 5;
     hipStream_t st = static_cast<hipStream_t>(stream);
     hipEvent_t ev[2] = {nullptr, nullptr};
     for (int k = 0; k < 2; ++k)
@@ -1075,40 +1080,44 @@ sqn_status sqn_tune_lanes_per_ray(sqn_caches* caches, const float* poses, int32_
             return fail(SQN_ERR_DEVICE, "hipEventCreate failed");
         }
     sqn_status s = SQN_OK;
-    int best = 0;
-    float best_ms = INFINITY;
-    for (int c = 0; c < n_cand && s == SQN_OK; ++c) {
+    float total_ms[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    auto render = [&](int c, int times) {
         caches->lanes = kCandidates[c];
         caches->centre = kCentre[c];
-        // kWarm untimed calls (code and caches warm), then kReps timed ones
-        for (int r = 0; r < kWarm && s == SQN_OK; ++r)
+        for (int r = 0; r < times && s == SQN_OK; ++r)
             s = render_common(caches, poses, n_poses, intrinsics, near_plane, far_plane, n_samples, rgb_out,
                               depth_out, nullptr, stream);
-        if (s != SQN_OK || n_poses == 0)
-            break;
-        hipError_t e = hipEventRecord(ev[0], st);
-        for (int r = 0; r < kReps && s == SQN_OK && e == hipSuccess; ++r)
-            s = render_common(caches, poses, n_poses, intrinsics, near_plane, far_plane, n_samples, rgb_out,
-                              depth_out, nullptr, stream);
-        if (s != SQN_OK)
-            break;
-        if (e == hipSuccess)
-            e = hipEventRecord(ev[1], st);
-        if (e == hipSuccess)
-            e = hipEventSynchronize(ev[1]);
-        float ms = 0.0f;
-        if (e == hipSuccess)
-            e = hipEventElapsedTime(&ms, ev[0], ev[1]);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();
-            s = fail(SQN_ERR_DEVICE, "timing the launch shapes failed: %s", hipGetErrorString(e));
-            break;
+    };
+    for (int c = 0; c < n_cand && s == SQN_OK; ++c)
+        render(c, kWarm);
+    for (int round = 0; round < kRounds && s == SQN_OK && n_poses > 0; ++round)
+        for (int c = 0; c < n_cand && s == SQN_OK; ++c) {
+            render(c, 1);
+            if (s != SQN_OK)
+                break;
+            hipError_t e = hipEventRecord(ev[0], st);
+            if (e == hipSuccess)
+                render(c, kReps);
+            if (s != SQN_OK)
+                break;
+            if (e == hipSuccess)
+                e = hipEventRecord(ev[1], st);
+            if (e == hipSuccess)
+                e = hipEventSynchronize(ev[1]);
+            float ms = 0.0f;
+            if (e == hipSuccess)
+                e = hipEventElapsedTime(&ms, ev[0], ev[1]);
+            if (e != hipSuccess) {
+                (void)hipGetLastError();
+                s = fail(SQN_ERR_DEVICE, "timing the launch shapes failed: %s", hipGetErrorString(e));
+                break;
+            }
+            total_ms[c] += ms;
         }
-        if (ms < best_ms) {
-            best_ms = ms;
+    int best = 0;
+    for (int c = 1; c < n_cand; ++c)
+        if (total_ms[c] < total_ms[best])
             best = c;
-        }
-    }
     (void)hipEventDestroy(ev[0]);
     (void)hipEventDestroy(ev[1]);
     if (s != SQN_OK || n_poses == 0) {

@@ -1426,10 +1426,13 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) 
     __shared__ RayGeom geom_smem[L >= 4 ? 64 : 1];
     int32_t view, tx, ty;
     if (P.block_order) {
-        // one view: blocks of 2 x 2 tiles from the centre outwards, the
-        // four workgroups of a block the ones 8 apart in dispatch order (one
-        // XCD, whose L2 then holds their shared texels); the grid covers
-        // whole blocks, and tiles past the image edge render nothing
+        // one view: blocks of 2 x 2 tiles from the centre outwards (the
+        // waves over a centred object carry the longest chains of samples
+        // and set the view's time, so they start first and the light edge
+        // tiles fill the end of the launch), the four workgroups of a block
+        // the ones 8 apart in dispatch order (one XCD, whose L2 then holds
+        // their shared texels); the grid covers whole blocks, and tiles past
+        // the image edge render nothing
         const int32_t bx = (P.tiles_x + 1) >> 1, by = (P.tiles_y + 1) >> 1;
         const int32_t bid = static_cast<int32_t>(blockIdx.x);
         int32_t blk = bid >> 2, sub = bid & 3;
@@ -1448,14 +1451,6 @@ __global__ __launch_bounds__(kBlockThreads, (occupancy<UT, DC, LIN, NDC, L>())) 
         const int32_t tr = tile - view * tiles_per_view;
         ty = tr / P.tiles_x;
         tx = tr - ty * P.tiles_x;
-    }
-    if (P.centre_out) {
-        // one view with one lane per ray: its time is set by the waves with
-        // the longest chains of samples, which sit over the middle of the
-        // image for a centred object, so those tiles go first and the light
-        // edge tiles fill the end of the launch
-        ty = centre_first(ty, P.tiles_y);
-        tx = centre_first(tx, P.tiles_x);
     }
     workgroup_rays<ST, UT, DC, STATS, L, SKIP, LIN, NDC>(P, view, tx, ty, beta_smem, lin_smem, queue_smem, qacc_smem,
                                                          geom_smem);

@@ -47,7 +47,6 @@ struct RenderParams {
     float leap_margin;        // texels a leap keeps from its square's edge
     int32_t tiles_x, tiles_y; // workgroup tiles per view
     int32_t n_groups;         // workgroups in the grid
-    int32_t centre_out;       // 1: tile rows and columns dealt from the image centre outwards
     int32_t block_order;      // 1: blocks of 2 x 2 tiles, each on one XCD, from the centre outwards
     // hybrid launch (one view): a centred rectangle of blocks of 16 x 16
     // pixels marched with four lanes per ray, the other blocks with one

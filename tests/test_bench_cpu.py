@@ -1,7 +1,6 @@
 """Host logic of bench.py (no GPU): the roofline arithmetic, the committed
 counter records against the current kernel sources, the single-GPU guard and
 the byte model of the method."""
-import dataclasses
 import hashlib
 import json
 import os
@@ -49,8 +48,11 @@ def test_committed_counters_describe_the_current_kernel(name):
 
 def test_counter_record_rejects_other_shapes_and_missing_files():
     assert bench.counter_record("no_such_workload") is None
-    # paper's record is of the hybrid launch, not of a one-lane kernel
-    assert bench.counter_record("paper", lanes=1) is None
+    # large's record is of the hybrid launch, paper's of the one-lane kernel
+    assert bench.counter_record("large", lanes=1) is None
+    assert bench.counter_record("large", lanes=-1) is not None
+    assert bench.counter_record("paper", lanes=-1) is None
+    assert bench.counter_record("paper", lanes=1) is not None
     # alt's record is of the four-lane kernel
     assert bench.counter_record("alt", lanes=8) is None
     assert bench.counter_record("alt", lanes=4) is not None
