@@ -628,7 +628,7 @@ __device__ __forceinline__ uint32_t fnv1a_word(uint32_t h, uint32_t x)
 // rounding).  Depth, sum w t, needs no records and stays in registers.
 constexpr uint32_t kQueue = 128;   // 63 waiting + 64 pushed at most
 
-constexpr bool defers_colour(int DC, bool LIN) { return !LIN && DC == 8; }
+constexpr bool defers_colour(int DC, bool LIN) { return !LIN && (DC == 8 || DC == 16); }
 
 struct ColourQueue {
     uint4* entries;        // [kQueue] wave-private ring: texel0 | slot << 26, texel1, texel2, w
@@ -643,9 +643,10 @@ struct ColourQueue {
 // in the one or two 64-byte segments of a record instead of one segment per
 // lane, which is what a gather costs the memory pipeline; the channel's
 // logit sums plane by plane in the order sample_colour uses.  That takes
-// four times the rounds, whose vector instructions the one-lane march
-// (already bound by vector-ALU issue with many views) cannot spare, so
-// QUADS is set for rays of four or eight lanes.  Otherwise, or in a wave at
+// four times the rounds, whose vector instructions the one-lane march at D
+// = 8 (bound by vector-ALU issue with many views) cannot spare, so QUADS is
+// set for rays of four or eight lanes and for D = 16, whose 96-byte records
+// leave the vector ALUs idle waiting for HBM.  Otherwise, or in a wave at
 // the image edge, one entry per lane.
 template <typename UT, int DC, bool LIN, int BS, bool QUADS>  // Eq. 4 only (LIN false)
 __device__ __forceinline__ void drain_colour(const RenderParams& P, const ColourQueue& cq, uint32_t& head,
@@ -1011,10 +1012,11 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
     const float leap_half = 0.5f + leap_margin;
     const int32_t n_p = P.n_p;
     const float hi_node = static_cast<float>(n_p - 1);
-    // Eq. 4 at D = 8 defers colour to the wave's queue (measured: 4-8%
-    // faster on every D = 8 workload; 10% slower on the HBM-bound D = 16
-    // one); Eq. 5 keeps a row of folded weights per ray in LDS and, like the
-    // other D, evaluates colour where the sample is found
+    // Eq. 4 at D = 8 and 16 defers colour to the wave's queue (measured:
+    // 4-8% faster on every D = 8 workload; at D = 16, drained by quads, 7%
+    // faster on the HBM-bound 1920x1080 view in its hybrid shape and 13%
+    // with one lane); Eq. 5 keeps a row of folded weights per ray in LDS
+    // and, like the other D, evaluates colour where the sample is found
     constexpr bool kDefer = defers_colour(DC, LIN);
     uint64_t tau = 0;              // optical depth before the chunk, 2^-32 units
     double acc_r = 0.0, acc_g = 0.0, acc_b = 0.0, acc_t = 0.0;
@@ -1249,13 +1251,13 @@ __device__ __forceinline__ void render_ray(const RenderParams& P, int32_t view, 
             // whole wave: count the pushes; evaluate 64 once they are waiting
             q_count += static_cast<uint32_t>(__builtin_popcountll(__builtin_amdgcn_ballot_w64(pushed)));
             if (q_count >= 64) {
-                drain_colour<UT, DC, LIN, BS, (L > 1)>(P, cq, q_head, 64);
+                drain_colour<UT, DC, LIN, BS, (L > 1 || DC == 16)>(P, cq, q_head, 64);
                 q_count -= 64;
             }
         }
     }
     if constexpr (kDefer)
-        drain_colour<UT, DC, LIN, BS, (L > 1)>(P, cq, q_head, q_count);
+        drain_colour<UT, DC, LIN, BS, (L > 1 || DC == 16)>(P, cq, q_head, q_count);
 
     // combine the lanes of the ray
     if constexpr (!kDefer) {
