@@ -178,3 +178,27 @@ def test_network_validation():
         nets.close()
     assert binding.lib.sqn_generate_caches(None, None, None, None, None, None) == binding.SQN_ERR_INVALID_ARG
     binding.lib.sqn_destroy_networks(None)
+
+
+def draw_gen_case(k):
+    """Generation case k from a generator seeded by k: grid sizes, D, depth
+    of both networks, encoding frequencies and the three storage types."""
+    rng = np.random.Generator(np.random.PCG64(9000 + k))
+    cfg = dataclasses.replace(
+        scenes.GEN_CONFIGS["gen_tiny"], name=f"gen_rand{k}", number=200 + k,
+        n_p=int(rng.integers(2, 81)), n_theta=int(rng.integers(2, 41)), n_phi=int(rng.integers(2, 41)),
+        D=int(rng.integers(1, 33)), pos_layers=int(rng.integers(1, 9)), dir_layers=int(rng.integers(1, 6)),
+        pos_freq=int(rng.integers(0, 13)), dir_freq=int(rng.integers(0, 7)))
+    dtypes = tuple(("f32", "f16")[int(rng.integers(0, 2))] for _ in range(3))
+    return cfg, dtypes
+
+
+@pytest.mark.parametrize("k", range(24))
+def test_generate_random_configurations(k):
+    """Seeded random combinations of grid sizes, D, network depths,
+    encoding frequencies and storage types, whole grids against the
+    oracle."""
+    cfg, dtypes = draw_gen_case(k)
+    g = scenes.make_gen_scene(cfg)
+    _full_compare(g, f"random {k} D={cfg.D} layers={cfg.pos_layers}/{cfg.dir_layers} "
+                     f"freq={cfg.pos_freq}/{cfg.dir_freq} {dtypes}", dtypes=dtypes)
