@@ -113,3 +113,15 @@ def test_generation_counter_record_matches_generate_hip():
     rec = bench.counter_record("gen_1k", kind="generate")
     assert rec is not None, "profiles/generate_traffic_gen_1k.json was taken on another generate.hip"
     assert rec["traffic_bytes_per_launch"] > 0
+
+
+@pytest.mark.parametrize("tag,workload,kernel", [("paper_hybrid1", "paper", "hybrid")])
+def test_alternative_shape_records_describe_the_current_kernel(tag, workload, kernel):
+    """Counter records of a workload in a shape other than its recorded one
+    (profiles/render_traffic_<tag>.json, cited beside the bench line) are of
+    the current render.hip too."""
+    raw = json.load(open(os.path.join(ROOT, "profiles", f"render_traffic_{tag}.json")))
+    src = open(os.path.join(ROOT, "paper_2204_02585_amd", "csrc", "render.hip"), "rb").read()
+    assert raw["render_hip_sha256_16"] == hashlib.sha256(src).hexdigest()[:16]
+    assert raw["workload"] == workload and kernel in raw["kernel"]
+    assert raw["td_busy_cycles_per_launch"] <= 256 * 2.4e3 * raw["kernel_us_trace"]
